@@ -1,0 +1,277 @@
+"""Float64 CPU oracle for the RelaxKV selective-repair hot path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this module: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it.  It shares no code with the HIP
+library (no kernels, headers, helpers, tables or pre/post-processing) and
+imports nothing from the product package.
+
+Every function is a plain, slow restatement of the paper's definitions in
+numpy float64 (arXiv 2609.33503, "RelaxKV: Recomputation Guided by the Query
+with Sparse Context Attention for Efficient KV Cache Reuse"):
+
+* ``score``        -- Sec. 3.2, layer-wise query-attention score a_{l,i}
+                      (pooled attention, MinMax-normalised per layer);
+                      first step of Algorithm 1.
+* ``anchor_count`` -- App. A.1, first equation: k = max(1, round(r T_c)).
+* ``select``       -- Sec. 3.2 / App. A.1 second equation: S_l = TopK_i(a_{l,i}, k),
+                      ties to the lowest position.
+* ``build_sets``   -- Sec. 3.2 / App. A.1 set equations: h_i, U, R_l; the compact
+                      index of App. A.2 ("compact execution"); the edge count
+                      E_unmasked and state cost of App. A.2.
+* ``sparse_attn``  -- Sec. 3.3 (C_l(p) = U cap {j <= p}) and Sec. 3.4 / App. A.2
+                      (mixed fresh/cached K~, V~ rule); the Full-Prefix Control
+                      of App. A.3 (Table "Controlled configurations") with
+                      ``mode="full"``.
+
+Readings where the paper is silent (each also listed in the design notes):
+
+* softmax domain of the scoring attention: the T_c cached keys only, unless
+  the caller supplies each query row's log-sum-exp (``row_lse``), in which case
+  A = exp(s - lse) with that normaliser;
+* softmax scale 1/sqrt(d) unless given;
+* GQA map: query head h reads KV head floor(h / (H / H_kv));
+* MinMax of a constant row is the all-zero row;
+* round() is round-half-to-even in IEEE double (Python's ``round``), then k is
+  clamped to [1, T_c];
+* equal scores are ordered by ascending position; -0.0 equals +0.0; a NaN
+  score is an error;
+* layers are 0-based, positions are context positions 0..T_c-1 only.
+
+Pins: every function is checked in ``tests/test_oracle_pins.py`` against
+something other than itself (closed forms, a hand-worked example, brute force
+on tiny inputs, torch's scaled_dot_product_attention in float64, and set
+invariants).
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+
+# ----------------------------------------------------------------------------
+# Scoring: Sec. 3.2 equation for a_{l,i}; Algorithm 1, scoring step.
+# ----------------------------------------------------------------------------
+
+def score(q, k_cache, softmax_scale=None, row_lse=None):
+    """Layer-wise pooled query attention over the cached context.
+
+    q        [L][Qn][H][d]     user-query rows per layer (already rotated).
+    k_cache  [L][H_kv][T_c][d] naive cached keys (already rotated).
+    row_lse  optional [L][Qn][H] natural-log normaliser of each query row.
+
+    For each layer l, head h and query token t the attention row is
+    A_l[h,t,:] = softmax_i(sigma <q_{l,t,h}, k_{l,g(h),i}>) over the T_c cached
+    keys (or exp(s - row_lse) when a normaliser is supplied).  The pooled score
+    is p_{l,i} = (1/(H Qn)) sum_h sum_t A_l[h,t,i] and a_{l,i} = MinMax_i(p_{l,i}).
+
+    Returns (a [L][T_c], p [L][T_c], lse [L][Qn][H]) in float64, where lse is
+    the log-sum-exp of each row's logits over the cached keys.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k_cache = np.asarray(k_cache, dtype=np.float64)
+    L, Qn, H, d = q.shape
+    H_kv, T_c = k_cache.shape[1], k_cache.shape[2]
+    if H % H_kv:
+        raise ValueError("H must be a multiple of H_kv")
+    G = H // H_kv
+    sigma = 1.0 / np.sqrt(d) if softmax_scale is None else float(softmax_scale)
+
+    p = np.zeros((L, T_c))
+    lse = np.zeros((L, Qn, H))
+    for l in range(L):
+        for h in range(H):
+            g = h // G
+            s = sigma * (q[l, :, h, :] @ k_cache[l, g].T)          # [Qn][T_c]
+            m = s.max(axis=1, keepdims=True)
+            z = np.exp(s - m).sum(axis=1, keepdims=True)
+            lse[l, :, h] = (m + np.log(z))[:, 0]
+            if row_lse is None:
+                A = np.exp(s - m) / z                               # softmax rows
+            else:
+                A = np.exp(s - np.asarray(row_lse, np.float64)[l, :, h][:, None])
+            p[l] += A.sum(axis=0)
+    p /= H * Qn
+
+    a = np.zeros_like(p)
+    for l in range(L):
+        lo, hi = p[l].min(), p[l].max()
+        if hi > lo:
+            a[l] = (p[l] - lo) / (hi - lo)
+        # else: constant row -> all zeros (MinMax of a constant)
+    return a, p, lse
+
+
+# ----------------------------------------------------------------------------
+# Selection: App. A.1, k and TopK equations; Algorithm 1, selection steps.
+# ----------------------------------------------------------------------------
+
+def anchor_count(ratio, T_c):
+    """k = max(1, round(r T_c)), clamped to T_c (Sec. 3.2, App. A.1)."""
+    ratio = float(ratio)
+    if not np.isfinite(ratio) or ratio < 0.0 or ratio > 1.0:
+        raise ValueError("anchor ratio must be a finite number in [0, 1]")
+    k = max(1, int(round(ratio * T_c)))
+    return min(k, int(T_c))
+
+
+def select(a, k):
+    """S_l = TopK_i(a_{l,i}, k) for every layer, returned sorted ascending.
+
+    Order is by descending score, then ascending position (lowest index wins
+    a tie).  -0.0 and +0.0 compare equal.  NaN is rejected.
+    """
+    a = np.asarray(a, dtype=np.float64)
+    if np.isnan(a).any():
+        raise ValueError("NaN score")
+    L, T_c = a.shape
+    out = np.empty((L, k), dtype=np.int64)
+    pos = np.arange(T_c)
+    for l in range(L):
+        # np.lexsort sorts by the last key first: primary -a (descending a),
+        # secondary the position (ascending).
+        order = np.lexsort((pos, -a[l]))
+        out[l] = np.sort(order[:k])
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Sets: h_i, U, R_l (Sec. 3.2 / App. A.1), compact indices and accounting
+# (App. A.2).
+# ----------------------------------------------------------------------------
+
+@dataclass
+class Sets:
+    T_c: int
+    k: int
+    anchors: np.ndarray                 # [L][k] sorted ascending
+    h: np.ndarray                       # [T_c] highest selected layer, -1 if none
+    U: np.ndarray                       # sorted union of anchors
+    cidx: np.ndarray                    # [T_c] compact index in U, -1 if not in U
+    R: list = field(default_factory=list)       # R[l]: sorted positions
+    R_u: list = field(default_factory=list)     # R_u[l][t]: compact index of R[l][t]
+    src: list = field(default_factory=list)     # src[l][c]: rank of U[c] in R[l] or -1
+    edges: np.ndarray = None            # [L] sum_{p in R_l} |C_l(p)|
+    edges_full: np.ndarray = None       # [L] sum_{p in R_l} (p + 1)
+
+    @property
+    def L(self):
+        return len(self.R)
+
+
+def build_sets(anchors, T_c):
+    """Highest selected layer, union, active targets and compact maps.
+
+    h_i = max{l : i in S_l}; U = union_l S_l; R_l = {i in U : h_i >= l}.
+    U is kept sorted and each position gets its compact index (App. A.2);
+    src[l][c] is the rank of U[c] within R_l (the row of the freshly
+    recomputed K/V), or -1 when U[c] is not active at layer l.
+    edges[l] = sum_{p in R_l} |C_l(p)| with C_l(p) = U cap {j <= p}
+    (App. A.2 edge count); edges_full[l] is the same count for the full causal
+    prefix, sum_{p in R_l} (p + 1).
+    """
+    anchors = np.asarray(anchors, dtype=np.int64)
+    L, k = anchors.shape
+    h = np.full(T_c, -1, dtype=np.int64)
+    for l in range(L):
+        h[anchors[l]] = np.maximum(h[anchors[l]], l)
+    U = np.flatnonzero(h >= 0)
+    cidx = np.full(T_c, -1, dtype=np.int64)
+    cidx[U] = np.arange(len(U))
+
+    R, R_u, src = [], [], []
+    edges = np.zeros(L, dtype=np.int64)
+    edges_full = np.zeros(L, dtype=np.int64)
+    for l in range(L):
+        R_l = U[h[U] >= l]
+        u_l = cidx[R_l]
+        s_l = np.full(len(U), -1, dtype=np.int64)
+        s_l[u_l] = np.arange(len(R_l))
+        R.append(R_l)
+        R_u.append(u_l)
+        src.append(s_l)
+        # |C_l(p)| = number of union positions <= p = compact index of p + 1.
+        edges[l] = int(np.sum(u_l + 1))
+        edges_full[l] = int(np.sum(R_l + 1))
+    return Sets(T_c=T_c, k=k, anchors=anchors, h=h, U=U, cidx=cidx,
+                R=R, R_u=R_u, src=src, edges=edges, edges_full=edges_full)
+
+
+# ----------------------------------------------------------------------------
+# Sparse-context attention: Sec. 3.3, Sec. 3.4 equation, App. A.2.
+# ----------------------------------------------------------------------------
+
+def sparse_attn(layer, sets, q_new, k_new, v_new, k_cache_l, v_cache_l,
+                softmax_scale=None, mode="union", targets=None):
+    """Attention of the active targets of one layer over their context.
+
+    q_new      [|R_l|][H][d]    fresh queries of the targets, rows in R_l order.
+    k_new/v_new[|R_l|][H_kv][d] fresh keys/values of the targets.
+    k_cache_l/v_cache_l [H_kv][T_c][d] naive cache of this layer.
+    mode       "union": target p attends to C_l(p) = U cap {j <= p} (RelaxKV);
+               "full":  target p attends to {j <= p} (Full-Prefix Control).
+    targets    optional iterable of ranks t in R_l to evaluate (default: all).
+
+    For every context position j the key/value is the fresh row when j is an
+    active target of this layer (j in R_l) and the naive cached row otherwise
+    (Sec. 3.4).  With O_{t,h} = sum_j softmax_j(sigma <q_{t,h}, K~_{j,g(h)}>) V~_{j,g(h)}.
+
+    Returns (O [n][H][d], lse [n][H]) in float64 for the requested targets.
+    """
+    q_new = np.asarray(q_new, dtype=np.float64)
+    k_new = np.asarray(k_new, dtype=np.float64)
+    v_new = np.asarray(v_new, dtype=np.float64)
+    k_cache_l = np.asarray(k_cache_l, dtype=np.float64)
+    v_cache_l = np.asarray(v_cache_l, dtype=np.float64)
+    R_l = sets.R[layer]
+    n_R = len(R_l)
+    if q_new.shape[0] != n_R or k_new.shape[0] != n_R or v_new.shape[0] != n_R:
+        raise ValueError("fresh rows must number |R_l|")
+    H, d = q_new.shape[1], q_new.shape[2]
+    H_kv = k_cache_l.shape[0]
+    G = H // H_kv
+    sigma = 1.0 / np.sqrt(d) if softmax_scale is None else float(softmax_scale)
+
+    # Rank of every position within R_l (-1 when not active at this layer).
+    rank = np.full(sets.T_c, -1, dtype=np.int64)
+    rank[R_l] = np.arange(n_R)
+
+    if mode == "union":
+        ctx_all = sets.U
+    elif mode == "full":
+        ctx_all = np.arange(sets.T_c)
+    else:
+        raise ValueError("mode must be 'union' or 'full'")
+
+    # K~, V~ over the candidate context positions, [H_kv][n_ctx][d]: fresh
+    # rows where the position is in R_l, naive cached rows elsewhere.
+    fresh = rank[ctx_all] >= 0
+    Kt = k_cache_l[:, ctx_all, :].copy()
+    Vt = v_cache_l[:, ctx_all, :].copy()
+    Kt[:, fresh, :] = np.transpose(k_new[rank[ctx_all[fresh]]], (1, 0, 2))
+    Vt[:, fresh, :] = np.transpose(v_new[rank[ctx_all[fresh]]], (1, 0, 2))
+
+    ts = range(n_R) if targets is None else list(targets)
+    O = np.zeros((len(ts), H, d))
+    lse = np.zeros((len(ts), H))
+    for n, t in enumerate(ts):
+        p = R_l[t]
+        m = int(np.searchsorted(ctx_all, p, side="right"))   # |{j in ctx : j <= p}|
+        for h in range(H):
+            g = h // G
+            s = sigma * (Kt[g, :m, :] @ q_new[t, h])           # [m]
+            mx = s.max()
+            e = np.exp(s - mx)
+            z = e.sum()
+            O[n, h] = (e / z) @ Vt[g, :m, :]
+            lse[n, h] = mx + np.log(z)
+    return O, lse
+
+
+def attention_flops(H, d, edges):
+    """Algorithmic attention FLOPs for a number of unmasked causal edges:
+    per edge and query head one d-long dot product (2d) and one d-long
+    weighted sum (2d)."""
+    return 4.0 * H * d * float(np.sum(edges))

@@ -1,0 +1,374 @@
+"""Pins of the float64 oracle against things other than itself.
+
+Closed forms, the hand-worked example under tests/golden/, brute force on tiny
+inputs, torch's scaled_dot_product_attention in float64, and the set
+invariants the method implies (Sec. 3.2 - 3.4, App. A).  No GPU needed.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+from hypothesis import given, settings
+from hypothesis import strategies as st
+
+from oracle import anchor_count, build_sets, score, select, sparse_attn
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ----------------------------------------------------------------------------
+# anchor budget k = max(1, round(r T_c))
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("r,T,k", [
+    (0.15, 1024, 154), (0.15, 8192, 1229), (0.05, 16384, 819), (0.15, 16384, 2458),
+    (0.30, 16384, 4915), (0.15, 32768, 4915),
+    # exact halves go to the even neighbour; k never drops below 1 or above T_c
+    (0.125, 20, 2), (0.375, 4, 2), (0.625, 4, 2), (0.5, 1, 1), (0.0, 50, 1), (1.0, 77, 77),
+])
+def test_anchor_count_closed_forms(r, T, k):
+    assert anchor_count(r, T) == k
+
+
+@pytest.mark.parametrize("r", [-0.01, 1.01, float("nan"), float("inf")])
+def test_anchor_count_rejects(r):
+    with pytest.raises(ValueError):
+        anchor_count(r, 100)
+
+
+# ----------------------------------------------------------------------------
+# hand-worked example (select, sets, attention)
+# ----------------------------------------------------------------------------
+
+def _hand():
+    with open(os.path.join(GOLDEN, "hand_example.json")) as f:
+        return json.load(f)
+
+
+def test_hand_example_select_and_sets():
+    ex = _hand()
+    k = anchor_count(ex["ratio"], ex["T_c"])
+    assert k == ex["k"]
+    S = select(np.array(ex["a"]), k)
+    assert S.tolist() == ex["anchors"]
+    s = build_sets(S, ex["T_c"])
+    assert s.h.tolist() == ex["h"]
+    assert s.U.tolist() == ex["U"]
+    assert [r.tolist() for r in s.R] == ex["R"]
+    assert [x.tolist() for x in s.src] == ex["src"]
+    assert s.edges.tolist() == ex["edges"]
+    assert s.edges_full.tolist() == ex["edges_full"]
+
+
+def test_hand_example_attention():
+    ex = _hand()
+    T = ex["T_c"]
+    s = build_sets(np.array(ex["anchors"]), T)
+    kc = np.zeros((1, T, 1))
+    vc = np.arange(T, dtype=np.float64).reshape(1, T, 1)
+    for case in ex["attention"]:
+        l = case["layer"]
+        R_l = s.R[l]
+        qn = np.ones((len(R_l), 1, 1))
+        kn = np.zeros((len(R_l), 1, 1))
+        vn = (R_l.astype(np.float64) + 100.0).reshape(-1, 1, 1)
+        t = int(np.flatnonzero(R_l == case["position"])[0])
+        O, _ = sparse_attn(l, s, qn, kn, vn, kc, vc, softmax_scale=1.0,
+                           mode=case["mode"], targets=[t])
+        assert O[0, 0, 0] == pytest.approx(case["out"], abs=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# score: closed forms, invariants, independent library routine
+# ----------------------------------------------------------------------------
+
+def test_score_closed_form_logs():
+    # one head, one query token, d = 1, sigma = 1, q = 1, keys = log(1..4):
+    # softmax = (1,2,3,4)/10, MinMax -> (0, 1/3, 2/3, 1).
+    q = np.ones((1, 1, 1, 1))
+    k = np.log(np.arange(1, 5, dtype=np.float64)).reshape(1, 1, 4, 1)
+    a, p, lse = score(q, k, softmax_scale=1.0)
+    np.testing.assert_allclose(p[0], [0.1, 0.2, 0.3, 0.4], atol=1e-15)
+    np.testing.assert_allclose(a[0], [0, 1 / 3, 2 / 3, 1], atol=1e-15)
+    assert lse[0, 0, 0] == pytest.approx(math.log(10.0), abs=1e-15)
+
+
+def test_score_degenerate_minmax_and_gqa_sharing():
+    # Two query heads share one KV head (G = 2) with q = (+1, -1) and keys
+    # (0, log 2): the rows are (1/3, 2/3) and (2/3, 1/3), the pooled score is
+    # (1/2, 1/2) -> constant -> a = 0 -> the tie rule picks position 0.
+    q = np.array([1.0, -1.0]).reshape(1, 1, 2, 1)
+    k = np.array([0.0, math.log(2.0)]).reshape(1, 1, 2, 1)
+    a, p, _ = score(q, k, softmax_scale=1.0)
+    np.testing.assert_allclose(p[0], [0.5, 0.5], atol=1e-15)
+    assert a[0].tolist() == [0.0, 0.0]
+    kk = anchor_count(0.2, 2)
+    assert kk == 1
+    assert select(a, kk).tolist() == [[0]]
+
+
+def test_score_equal_keys_select_first_k():
+    rng = np.random.default_rng(0)
+    q = rng.standard_normal((2, 3, 4, 8))
+    k = np.broadcast_to(rng.standard_normal((1, 2, 1, 8)), (2, 2, 30, 8)).copy()
+    a, _, _ = score(q, k)
+    assert np.all(a == 0.0)
+    assert select(a, 5).tolist() == [list(range(5))] * 2
+
+
+def _rand_score_inputs(seed, L=2, Qn=3, H=4, H_kv=2, T=37, d=8):
+    rng = np.random.default_rng(seed)
+    return rng.standard_normal((L, Qn, H, d)), rng.standard_normal((L, H_kv, T, d))
+
+
+def test_score_pooled_mass_is_one():
+    # every softmax row sums to 1, so the pooled mean over H*Qn rows sums to 1
+    q, k = _rand_score_inputs(1)
+    _, p, _ = score(q, k)
+    np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-13)
+
+
+def test_score_matches_brute_force_loops():
+    q, k = _rand_score_inputs(2, L=1, Qn=2, H=4, H_kv=2, T=9, d=3)
+    a, p, _ = score(q, k)
+    L, Qn, H, d = q.shape
+    T = k.shape[2]
+    pb = [0.0] * T
+    for h in range(H):
+        g = h // 2
+        for t in range(Qn):
+            logits = [sum(q[0, t, h, e] * k[0, g, i, e] for e in range(d)) / math.sqrt(d)
+                      for i in range(T)]
+            z = sum(math.exp(x) for x in logits)
+            for i in range(T):
+                pb[i] += math.exp(logits[i]) / z / (H * Qn)
+    np.testing.assert_allclose(p[0], pb, rtol=1e-12)
+    lo, hi = min(pb), max(pb)
+    np.testing.assert_allclose(a[0], [(x - lo) / (hi - lo) for x in pb], atol=1e-12)
+
+
+def test_score_matches_sdpa_attention_weights():
+    # scaled_dot_product_attention with V = identity returns the attention
+    # weights themselves; enable_gqa maps query head h to KV head h // G.
+    q, k = _rand_score_inputs(3, L=2, Qn=5, H=6, H_kv=2, T=23, d=16)
+    _, p, _ = score(q, k)
+    for l in range(q.shape[0]):
+        qt = torch.from_numpy(q[l]).permute(1, 0, 2)[None]            # [1][H][Qn][d]
+        kt = torch.from_numpy(k[l])[None]                               # [1][H_kv][T][d]
+        eye = torch.eye(k.shape[2], dtype=torch.float64).expand(1, k.shape[1], -1, -1)
+        A = torch.nn.functional.scaled_dot_product_attention(qt, kt, eye, enable_gqa=True)
+        np.testing.assert_allclose(p[l], A.mean(dim=(0, 1, 2)).numpy(), atol=1e-14)
+
+
+def test_score_supplied_lse():
+    q, k = _rand_score_inputs(4)
+    a, p, lse = score(q, k)
+    a2, p2, _ = score(q, k, row_lse=lse)
+    np.testing.assert_allclose(p2, p, rtol=1e-12)
+    # a larger normaliser (the query's own tokens in a real forward) scales p
+    # by exp(-c) and leaves the MinMax-normalised score unchanged
+    a3, p3, _ = score(q, k, row_lse=lse + 0.7)
+    np.testing.assert_allclose(p3, p * math.exp(-0.7), rtol=1e-12)
+    np.testing.assert_allclose(a3, a, atol=1e-12)
+
+
+def test_score_permutation_equivariance():
+    q, k = _rand_score_inputs(5)
+    perm = np.random.default_rng(9).permutation(k.shape[2])
+    a, p, _ = score(q, k)
+    a2, p2, _ = score(q, k[:, :, perm, :])
+    np.testing.assert_allclose(p2, p[:, perm], rtol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# select: brute force, ties, -0.0, NaN, invariance
+# ----------------------------------------------------------------------------
+
+def _brute_topk(row, k):
+    order = sorted(range(len(row)), key=lambda i: (-row[i], i))
+    return sorted(order[:k])
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.integers(1, 4), st.integers(1, 40), st.data())
+def test_select_brute_force_with_ties(L, T, data):
+    vals = data.draw(st.lists(st.sampled_from([0.0, -0.0, 0.25, 0.5, 0.75, 1.0, 0.1]),
+                              min_size=L * T, max_size=L * T))
+    a = np.array(vals).reshape(L, T)
+    k = data.draw(st.integers(1, T))
+    S = select(a, k)
+    for l in range(L):
+        assert S[l].tolist() == _brute_topk([0.0 if x == 0 else x for x in a[l]], k)
+
+
+def test_select_negative_zero_ties_positive_zero():
+    a = np.array([[-0.0, 0.0, -0.0, 0.0]])
+    assert select(a, 2).tolist() == [[0, 1]]
+
+
+def test_select_rejects_nan():
+    with pytest.raises(ValueError):
+        select(np.array([[0.1, float("nan")]]), 1)
+
+
+def test_select_positive_affine_invariance():
+    rng = np.random.default_rng(6)
+    a = rng.integers(0, 16, size=(3, 50)) / 8.0          # exact under x -> 2x + 0.5
+    for k in (1, 7, 25, 50):
+        assert np.array_equal(select(a, k), select(2.0 * a + 0.5, k))
+
+
+# ----------------------------------------------------------------------------
+# sets: invariants of h, U, R_l and the edge counts
+# ----------------------------------------------------------------------------
+
+def _random_anchors(rng, L, T, k):
+    return np.stack([np.sort(rng.choice(T, size=k, replace=False)) for _ in range(L)])
+
+
+@settings(max_examples=80, deadline=None)
+@given(st.integers(1, 5), st.integers(1, 60), st.integers(0, 2**31 - 1), st.data())
+def test_sets_invariants(L, T, seed, data):
+    k = data.draw(st.integers(1, T))
+    S = _random_anchors(np.random.default_rng(seed), L, T, k)
+    s = build_sets(S, T)
+    union = set()
+    for l in range(L):
+        union |= set(S[l].tolist())
+    assert s.U.tolist() == sorted(union)                          # U = union of S_l
+    assert len(s.R) == L
+    for i in range(T):                                            # active exactly up to h_i
+        for l in range(L):
+            assert (i in set(s.R[l].tolist())) == (s.h[i] >= 0 and l <= s.h[i])
+    assert s.R[0].tolist() == s.U.tolist()                        # R_0 = U
+    assert s.R[L - 1].tolist() == S[L - 1].tolist()               # R_{L-1} = S_{L-1}
+    for l in range(L):
+        assert len(S[l]) == k
+        assert set(S[l].tolist()) <= set(s.R[l].tolist())          # S_l within R_l
+        if l + 1 < L:
+            assert set(s.R[l + 1].tolist()) <= set(s.R[l].tolist())   # nested
+        assert np.all(np.diff(s.R[l]) > 0)
+        # src: rank of U[c] in R_l, or -1
+        for c, pos in enumerate(s.U.tolist()):
+            hits = np.flatnonzero(s.R[l] == pos)
+            assert s.src[l][c] == (hits[0] if len(hits) else -1)
+        # edges by counting |C_l(p)| directly
+        e = sum(sum(1 for j in s.U.tolist() if j <= p) for p in s.R[l].tolist())
+        assert s.edges[l] == e
+        assert s.edges_full[l] == sum(p + 1 for p in s.R[l].tolist())
+        assert s.edges[l] <= s.edges_full[l]
+        full_prefix_in_U = all(set(range(p + 1)) <= union for p in s.R[l].tolist())
+        assert (s.edges[l] == s.edges_full[l]) == full_prefix_in_U
+    assert sum(len(r) for r in s.R) == int(np.sum(s.h[s.U] + 1))   # state count
+
+
+# ----------------------------------------------------------------------------
+# sparse attention: brute force with an explicit dense mask, causal reduction
+# ----------------------------------------------------------------------------
+
+def _brute_attention(l, S, T, qn, kn, vn, kc, vc, sigma, mode):
+    """Dense masked attention over all T positions, evaluating the context and
+    the mixed fresh/cached rule literally for every (target, position) pair."""
+    L = len(S)
+    U = set()
+    for x in S:
+        U |= set(int(i) for i in x)
+    h = {i: max(ll for ll in range(L) if i in set(S[ll].tolist())) for i in U}
+    R = sorted(i for i in U if h[i] >= l)
+    rank = {p: t for t, p in enumerate(R)}
+    H, d = qn.shape[1], qn.shape[2]
+    G = H // kc.shape[0]
+    O = np.zeros((len(R), H, d))
+    lse = np.zeros((len(R), H))
+    for t, p in enumerate(R):
+        for hh in range(H):
+            g = hh // G
+            logits = np.full(T, -np.inf)
+            vals = np.zeros((T, d))
+            for j in range(T):
+                in_ctx = (j in U and j <= p) if mode == "union" else (j <= p)
+                if not in_ctx:
+                    continue
+                fresh = j in rank                    # j in R_l (and in the context)
+                kj = kn[rank[j], g] if fresh else kc[g, j]
+                vals[j] = vn[rank[j], g] if fresh else vc[g, j]
+                logits[j] = sigma * float(np.dot(qn[t, hh], kj))
+            m = logits.max()
+            w = np.exp(logits - m)
+            O[t, hh] = (w / w.sum()) @ vals
+            lse[t, hh] = m + math.log(w.sum())
+    return np.array(R), O, lse
+
+
+@pytest.mark.parametrize("seed,L,T,k,mode", [(0, 3, 40, 6, "union"), (1, 2, 33, 3, "union"),
+                                             (2, 3, 40, 6, "full"), (3, 4, 25, 1, "union")])
+def test_attention_brute_force(seed, L, T, k, mode):
+    rng = np.random.default_rng(seed)
+    H, H_kv, d = 4, 2, 8
+    S = _random_anchors(rng, L, T, k)
+    s = build_sets(S, T)
+    for l in range(L):
+        n = len(s.R[l])
+        qn = rng.standard_normal((n, H, d))
+        kn = rng.standard_normal((n, H_kv, d))
+        vn = rng.standard_normal((n, H_kv, d))
+        kc = rng.standard_normal((H_kv, T, d))
+        vc = rng.standard_normal((H_kv, T, d))
+        O, lse = sparse_attn(l, s, qn, kn, vn, kc, vc, mode=mode)
+        R, Ob, lseb = _brute_attention(l, S, T, qn, kn, vn, kc, vc, 1 / math.sqrt(d), mode)
+        assert R.tolist() == s.R[l].tolist()
+        np.testing.assert_allclose(O, Ob, atol=1e-12)
+        np.testing.assert_allclose(lse, lseb, atol=1e-12)
+        # softmax rows sum to 1: exp(logits - lse) over the context
+        t = n - 1
+        p = s.R[l][t]
+        ctx = s.U[s.U <= p] if mode == "union" else np.arange(p + 1)
+        rank = {int(x): i for i, x in enumerate(s.R[l])}
+        Krows = np.stack([kn[rank[j]] if j in rank else kc[:, j] for j in ctx.tolist()])
+        for hh in range(H):
+            w = np.exp(Krows[:, hh // 2] @ qn[t, hh] / math.sqrt(d) - lse[t, hh])
+            assert w.sum() == pytest.approx(1.0, abs=1e-12)
+
+
+def test_attention_full_union_is_causal_sdpa():
+    # every position an anchor of every layer -> U = R_l = all positions, and
+    # sparse-context attention is ordinary causal GQA self-attention on the
+    # fresh rows.
+    rng = np.random.default_rng(7)
+    L, T, H, H_kv, d = 2, 29, 6, 2, 16
+    S = np.tile(np.arange(T), (L, 1))
+    s = build_sets(S, T)
+    qn = rng.standard_normal((T, H, d))
+    kn = rng.standard_normal((T, H_kv, d))
+    vn = rng.standard_normal((T, H_kv, d))
+    kc = rng.standard_normal((H_kv, T, d))          # never read
+    vc = rng.standard_normal((H_kv, T, d))
+    for mode in ("union", "full"):
+        O, _ = sparse_attn(1, s, qn, kn, vn, kc, vc, mode=mode)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(qn).permute(1, 0, 2)[None],
+            torch.from_numpy(kn).permute(1, 0, 2)[None],
+            torch.from_numpy(vn).permute(1, 0, 2)[None], is_causal=True, enable_gqa=True)
+        np.testing.assert_allclose(O, ref[0].permute(1, 0, 2).numpy(), atol=1e-12)
+
+
+def test_attention_union_equals_full_prefix_when_union_covers_all():
+    # S_0, S_1, S_2 partition the positions: U = everything, but R_l shrinks.
+    rng = np.random.default_rng(8)
+    T, H, H_kv, d = 12, 2, 1, 4
+    S = np.arange(T).reshape(3, 4)
+    s = build_sets(S, T)
+    assert s.U.tolist() == list(range(T))
+    kc = rng.standard_normal((H_kv, T, d))
+    vc = rng.standard_normal((H_kv, T, d))
+    for l in range(3):
+        n = len(s.R[l])
+        qn, kn, vn = (rng.standard_normal((n, hh, d)) for hh in (H, H_kv, H_kv))
+        Ou, lu = sparse_attn(l, s, qn, kn, vn, kc, vc, mode="union")
+        Of, lf = sparse_attn(l, s, qn, kn, vn, kc, vc, mode="full")
+        np.testing.assert_allclose(Ou, Of, atol=1e-14)
+        np.testing.assert_allclose(lu, lf, atol=1e-14)
