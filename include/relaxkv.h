@@ -1,0 +1,218 @@
+/*
+ * relaxkv.h -- C ABI of the RelaxKV selective-repair hot path on MI355X (gfx950).
+ *
+ * RelaxKV (arXiv 2609.33503) repairs a position-independent chunk KV cache for
+ * one user query.  Its problem statement (Sec. 3.1): given the naive cache
+ * K^naive, a query q and an anchor ratio r, choose per-layer repair targets and
+ * a shared recomputation context, and recompute the targets' attention over
+ * that context.  This library implements the per-layer hot path of that
+ * repair as four calls, in order:
+ *
+ *   relaxkv_score       pooled, MinMax-normalised query attention a_{l,i}  (Sec. 3.2)
+ *   relaxkv_select      S_l = TopK_i(a_{l,i}, k), k = max(1, round(r T_c)) (Sec. 3.2, App. A.1)
+ *   relaxkv_build_sets  h_i, U, R_l, compact maps, edge counts          (Sec. 3.2, App. A.1-A.2)
+ *   relaxkv_sparse_attn attention of R_l over C_l(p) = U cap {j <= p}
+ *                       with the mixed fresh/cached K~, V~ rule          (Sec. 3.3, 3.4, App. A.2)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Device pointers are HIP device memory of the current device; host
+ *   pointers are marked "host".  The caller owns every buffer: the library
+ *   never allocates, frees or retains a pointer past the call.
+ * - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *   stream) unless it says it synchronises.  Inputs must stay valid and
+ *   unmodified until the stream reaches the call.
+ * - Arguments are validated on the host before anything is enqueued.  On any
+ *   error code nothing is enqueued and no output is touched.
+ * - Arrays are row-major with the last index contiguous and no padding.
+ *   Element types: int32 for indices and counts, int64 for edge counts,
+ *   float32 for scores and log-sum-exp values, and `dtype` (bfloat16 or
+ *   float32) for Q/K/V and attention outputs.
+ * - Layers are 0-based; positions are context positions 0 .. T_c-1 (the
+ *   query tokens are never targets or context).
+ * - Calls are stateless and reentrant; two calls that write the same buffers
+ *   must be ordered by the caller.
+ */
+#ifndef RELAXKV_H
+#define RELAXKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t relaxkv_status;
+#define RELAXKV_OK            0
+#define RELAXKV_EINVAL       -1  /* null pointer, bad dimension, ratio not in [0,1], layer out of range, NaN score */
+#define RELAXKV_ENOSPACE     -2  /* caller buffer smaller than the size query reports */
+#define RELAXKV_EUNSUPPORTED -3  /* head_dim, dtype or head layout this build has no kernel for */
+#define RELAXKV_EDEVICE      -4  /* a HIP runtime call or kernel launch failed */
+
+#define RELAXKV_DTYPE_F32  0
+#define RELAXKV_DTYPE_BF16 1
+
+#define RELAXKV_CONTEXT_UNION 0  /* C_l(p) = U cap {j <= p} (RelaxKV, Sec. 3.3) */
+#define RELAXKV_CONTEXT_FULL  1  /* {j <= p}: Full-Prefix Control (App. A.3) */
+
+/* Limits of this build (checked by relaxkv_validate). */
+#define RELAXKV_MAX_LAYERS 1024
+#define RELAXKV_MAX_TC     (1 << 22)
+
+/*
+ * The problem every call describes.
+ *   L, T_c     layers and context tokens; n_query query tokens; H query heads,
+ *              H_kv key/value heads (H % H_kv == 0; query head h reads KV head
+ *              h / (H / H_kv)); d head dimension (64 or 128).
+ *   softmax_scale  sigma in softmax(sigma q.k); <= 0 selects 1/sqrt(d).
+ *   anchor_ratio   r in [0, 1].
+ *   q          device [L][n_query][H][d]  the user query's rows (already rotated
+ *              at their global positions).
+ *   k_cache    device [L][H_kv][T_c][d]   naive cached keys (already rotated).
+ *   v_cache    device [L][H_kv][T_c][d]   naive cached values.
+ *   q_lse      optional device [L][n_query][H] float32: natural-log normaliser of
+ *              each query row from the caller's own query forward.  When NULL
+ *              the scoring softmax runs over the T_c cached keys only and
+ *              relaxkv_score computes the normaliser itself (two passes over K);
+ *              when given, relaxkv_score reads K once.
+ */
+typedef struct relaxkv_problem {
+    int32_t L, T_c, n_query, H, H_kv, d;
+    int32_t dtype;
+    float softmax_scale;
+    double anchor_ratio;
+    const void* q;
+    const void* k_cache;
+    const void* v_cache;
+    const float* q_lse;
+} relaxkv_problem;
+
+/*
+ * The index sets of one request, carved by relaxkv_sets_bind out of one
+ * caller-owned device buffer.  All pointers are device pointers.
+ *   anchors  [L][k]        S_l, ascending positions.
+ *   h        [T_c]         highest selected layer h_i, -1 when i is in no S_l.
+ *   U        [T_c]         U sorted ascending in the first |U| entries.
+ *   cidx     [T_c]         compact index of position i in U, -1 if i not in U.
+ *   R_off    [L+1]         R_l occupies entries R_off[l] .. R_off[l+1]-1 of R_idx/R_u.
+ *   R_idx    [L*T_c]       positions of R_l, ascending (CSR over layers).
+ *   R_u      [L*T_c]       compact index (in U) of each R_idx entry.
+ *   src      [L][T_c]      src[l*T_c + c] = rank of U[c] within R_l (its row in the
+ *                          fresh K/V of layer l), or -1 (cached row), c < |U|.
+ *   counts   [L+2]         counts[0] = |U|; counts[1+l] = |R_l|; counts[L+1] = error
+ *                          word (nonzero when a NaN score reached relaxkv_select).
+ *   edges    [2L]          edges[l] = sum_{p in R_l} |C_l(p)| (App. A.2 edge count);
+ *                          edges[L+l] = sum_{p in R_l} (p+1), the full-prefix count.
+ *   k        the anchor budget k = max(1, round(r T_c)), computed on the host.
+ */
+typedef struct relaxkv_sets {
+    int32_t L, T_c, k;
+    int32_t* anchors;
+    int32_t* h;
+    int32_t* U;
+    int32_t* cidx;
+    int32_t* R_off;
+    int32_t* R_idx;
+    int32_t* R_u;
+    int32_t* src;
+    int32_t* counts;
+    int64_t* edges;
+} relaxkv_sets;
+
+/* Text of a status code (static storage). */
+const char* relaxkv_status_string(relaxkv_status s);
+
+/* Host only.  k = max(1, round(r T_c)) with round-half-to-even in double,
+ * clamped to T_c (Sec. 3.2, App. A.1).  Returns k >= 1, or RELAXKV_EINVAL when
+ * r is not a finite number in [0, 1] or T_c < 1. */
+int32_t relaxkv_anchor_count(double anchor_ratio, int32_t T_c);
+
+/* Host only.  Checks dimensions, pointers, dtype and the ratio of `p`. */
+relaxkv_status relaxkv_validate(const relaxkv_problem* p);
+
+/* Host only.  Device scratch bytes relaxkv_score needs (0 when p is invalid). */
+size_t relaxkv_score_workspace_bytes(const relaxkv_problem* p);
+
+/* Host only.  Device bytes of the set arrays of relaxkv_sets (0 when p is invalid). */
+size_t relaxkv_sets_bytes(const relaxkv_problem* p);
+
+/* Host only.  Fills *out with L, T_c, k and pointers carved out of the device
+ * buffer `dev_buf` of `bytes` bytes (256-byte aligned sub-arrays).
+ * RELAXKV_ENOSPACE when bytes < relaxkv_sets_bytes(p). */
+relaxkv_status relaxkv_sets_bind(const relaxkv_problem* p, void* dev_buf, size_t bytes,
+                                 relaxkv_sets* out);
+
+/*
+ * Layer-wise query-attention score (Sec. 3.2 equation; first step of
+ * Algorithm 1).  For every layer l, query head h and query token t the row
+ * A_l[h,t,:] = softmax_i(sigma <q_{l,t,h}, k_{l,h/G,i}>) over the T_c cached keys
+ * (or exp(s - q_lse) with a supplied normaliser); then
+ *   p_{l,i} = (1/(H n_query)) sum_{h,t} A_l[h,t,i],  a_{l,i} = MinMax_i(p_{l,i}),
+ * and a constant row maps to all zeros.
+ *   ws       device scratch of ws_bytes >= relaxkv_score_workspace_bytes(p).
+ *   scores   device out [L][T_c] float32, a_{l,i} in [0, 1].
+ * Reads q, k_cache and (optionally) q_lse of `p`; never reads v_cache.
+ */
+relaxkv_status relaxkv_score(const relaxkv_problem* p, void* ws, size_t ws_bytes,
+                             float* scores, void* stream);
+
+/*
+ * Per-layer top-k anchor selection (Sec. 3.2, App. A.1 TopK equation).
+ * S_l holds the k positions with the largest scores[l][i]; equal scores go to
+ * the lower position; -0.0 equals +0.0.  Writes s->anchors[l][0..k-1]
+ * ascending and clears s->counts[L+1]; a NaN score sets that error word
+ * (read it with relaxkv_counts_to_host) and leaves that layer's anchors
+ * unspecified.
+ *   scores   device [L][T_c] float32 (any finite values).
+ *   s        sets bound for the same problem (s->k from relaxkv_sets_bind).
+ */
+relaxkv_status relaxkv_select(const relaxkv_problem* p, const float* scores,
+                              const relaxkv_sets* s, void* stream);
+
+/*
+ * Repair schedule and compact context (Sec. 3.2 set equations, App. A.1-A.2):
+ *   h_i = max{l : i in S_l},  U = union_l S_l,  R_l = {i in U : h_i >= l},
+ * the compact index of every position in U, the per-layer source map src, the
+ * CSR lists R_idx/R_u, counts and edge counts.  Reads s->anchors (ascending
+ * rows, entries in [0, T_c)); writes every other array of `s`.
+ */
+relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, const relaxkv_sets* s,
+                                  void* stream);
+
+/*
+ * Sparse-context causal attention of layer `layer` (Sec. 3.3-3.4, App. A.2;
+ * Algorithm 1, attention step).  For every active target t (position
+ * p = R_idx[R_off[l] + t]) and query head h:
+ *   O_{t,h} = sum_{j in C} softmax_j(sigma <q_new_{t,h}, K~_j>) V~_j
+ * over C = C_l(p) = U cap {j <= p} (context_mode RELAXKV_CONTEXT_UNION) or
+ * {j <= p} (RELAXKV_CONTEXT_FULL), where K~_j, V~_j are the fresh row of j when
+ * j is in R_l and the naive cached row of j otherwise, read from KV head
+ * h / (H / H_kv).
+ *   q_new    device [|R_l|][H][d]     fresh queries, rows in R_l order.
+ *   k_new    device [|R_l|][H_kv][d]  fresh keys, rows in R_l order.
+ *   v_new    device [|R_l|][H_kv][d]  fresh values, rows in R_l order.
+ *   out      device out [|R_l|][H][d] dtype: attention output before o_proj.
+ *   lse_out  optional device out [|R_l|][H] float32: natural-log normaliser.
+ * |R_l| is read on the device from s->counts; the host needs no count.  The
+ * naive cache of the layer is read from p->k_cache / p->v_cache.
+ */
+relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets* s,
+                                   int32_t layer, const void* q_new, const void* k_new,
+                                   const void* v_new, void* out, float* lse_out,
+                                   int32_t context_mode, void* stream);
+
+/*
+ * Synchronising.  Copies s->counts ([L+2] int32) to host_counts and, when
+ * host_edges is not NULL, s->edges ([2L] int64) to host_edges, after all work
+ * queued on `stream`.  Returns RELAXKV_EINVAL when the device error word is
+ * set (a NaN score reached relaxkv_select), RELAXKV_EDEVICE on a HIP error.
+ */
+relaxkv_status relaxkv_counts_to_host(const relaxkv_sets* s, int32_t* host_counts,
+                                      int64_t* host_edges, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RELAXKV_H */

@@ -1,0 +1,39 @@
+// Internal declarations shared by the host C ABI and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "relaxkv.h"
+
+namespace relaxkv {
+
+// Scratch layout of relaxkv_score (offsets in bytes from the workspace base).
+struct ScoreWorkspace {
+    size_t part_off;    // float [L][n_part][T_c]   per-KV-head pooled partial sums
+    size_t stats_off;   // float2 [L][H_kv][n_split][rows_pad] (max, sum) per key split, log2 units
+    size_t lse_off;     // float [L][H_kv][rows_pad] row log2-sum-exp
+    size_t total;
+    int n_part;         // partial slices summed by the finaliser
+    int n_split;        // key splits of the row-statistics pass
+    int rows_pad;       // n_query * G rounded up to a multiple of 32
+};
+
+ScoreWorkspace score_workspace_layout(const relaxkv_problem& p);
+
+// Kernel launchers (each returns hipSuccess or the launch error).
+hipError_t launch_score(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws,
+                        float* scores, hipStream_t st);
+hipError_t launch_select(const relaxkv_problem& p, const float* scores,
+                         const relaxkv_sets& s, hipStream_t st);
+hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s,
+                             hipStream_t st);
+hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
+                              const void* q_new, const void* k_new, const void* v_new,
+                              void* out, float* lse_out, int context_mode, hipStream_t st);
+
+// Tile constants of the bf16 MFMA attention kernel.
+constexpr int kAttnRows = 128;      // (target, head) rows per workgroup: 4 waves x 32
+constexpr int kAttnKeys = 64;       // keys per LDS tile
+
+}  // namespace relaxkv

@@ -1,0 +1,186 @@
+// Host side of the C ABI: validation, buffer sizing and carving, launches.
+// Nothing here allocates device memory; every buffer belongs to the caller.
+
+#include <math.h>
+#include <string.h>
+
+#include "internal.h"
+
+using namespace relaxkv;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool dims_ok(const relaxkv_problem* p) {
+    return p->L >= 1 && p->L <= RELAXKV_MAX_LAYERS && p->T_c >= 1 && p->T_c <= RELAXKV_MAX_TC &&
+           p->n_query >= 1 && p->n_query <= 4096 && p->H >= 1 && p->H <= 1024 &&
+           p->H_kv >= 1 && p->H % p->H_kv == 0;
+}
+
+// Byte sizes of the set arrays, in carving order.
+struct SetsLayout {
+    size_t anchors, h, U, cidx, R_off, R_idx, R_u, src, counts, edges, total;
+};
+
+SetsLayout sets_layout(const relaxkv_problem* p, int32_t k) {
+    SetsLayout s;
+    const size_t L = (size_t)p->L, T = (size_t)p->T_c;
+    s.anchors = align_up(L * (size_t)k * 4);
+    s.h = align_up(T * 4);
+    s.U = align_up(T * 4);
+    s.cidx = align_up(T * 4);
+    s.R_off = align_up((L + 1) * 4);
+    s.R_idx = align_up(L * T * 4);
+    s.R_u = align_up(L * T * 4);
+    s.src = align_up(L * T * 4);
+    s.counts = align_up((L + 2) * 4);
+    s.edges = align_up(2 * L * 8);
+    s.total = s.anchors + s.h + s.U + s.cidx + s.R_off + s.R_idx + s.R_u + s.src + s.counts +
+              s.edges;
+    return s;
+}
+
+bool sets_match(const relaxkv_problem* p, const relaxkv_sets* s) {
+    return s && s->L == p->L && s->T_c == p->T_c &&
+           s->k == relaxkv_anchor_count(p->anchor_ratio, p->T_c) && s->anchors && s->h &&
+           s->U && s->cidx && s->R_off && s->R_idx && s->R_u && s->src && s->counts &&
+           s->edges;
+}
+
+relaxkv_status from_hip(hipError_t e) { return e == hipSuccess ? RELAXKV_OK : RELAXKV_EDEVICE; }
+
+}  // namespace
+
+extern "C" {
+
+const char* relaxkv_status_string(relaxkv_status s) {
+    switch (s) {
+        case RELAXKV_OK: return "ok";
+        case RELAXKV_EINVAL: return "invalid argument";
+        case RELAXKV_ENOSPACE: return "buffer too small";
+        case RELAXKV_EUNSUPPORTED: return "unsupported shape or dtype";
+        case RELAXKV_EDEVICE: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+int32_t relaxkv_anchor_count(double r, int32_t T_c) {
+    if (!isfinite(r) || r < 0.0 || r > 1.0 || T_c < 1) return RELAXKV_EINVAL;
+    // round-half-to-even in double (the default rounding mode of nearbyint)
+    double k = nearbyint(r * (double)T_c);
+    if (k < 1.0) k = 1.0;
+    if (k > (double)T_c) k = (double)T_c;
+    return (int32_t)k;
+}
+
+relaxkv_status relaxkv_validate(const relaxkv_problem* p) {
+    if (!p) return RELAXKV_EINVAL;
+    if (!dims_ok(p)) return RELAXKV_EINVAL;
+    if (!p->q || !p->k_cache || !p->v_cache) return RELAXKV_EINVAL;
+    if (isnan(p->softmax_scale) || isinf(p->softmax_scale)) return RELAXKV_EINVAL;
+    if (relaxkv_anchor_count(p->anchor_ratio, p->T_c) < 1) return RELAXKV_EINVAL;
+    if (p->dtype != RELAXKV_DTYPE_F32 && p->dtype != RELAXKV_DTYPE_BF16)
+        return RELAXKV_EUNSUPPORTED;
+    if (p->d != 64 && p->d != 128) return RELAXKV_EUNSUPPORTED;
+    // The bf16 attention tile packs whole GQA groups into 128 rows.
+    if (p->dtype == RELAXKV_DTYPE_BF16 && p->H / p->H_kv > kAttnRows) return RELAXKV_EUNSUPPORTED;
+    return RELAXKV_OK;
+}
+
+size_t relaxkv_score_workspace_bytes(const relaxkv_problem* p) {
+    if (relaxkv_validate(p) != RELAXKV_OK) return 0;
+    return score_workspace_layout(*p).total;
+}
+
+size_t relaxkv_sets_bytes(const relaxkv_problem* p) {
+    if (relaxkv_validate(p) != RELAXKV_OK) return 0;
+    return sets_layout(p, relaxkv_anchor_count(p->anchor_ratio, p->T_c)).total;
+}
+
+relaxkv_status relaxkv_sets_bind(const relaxkv_problem* p, void* dev_buf, size_t bytes,
+                                 relaxkv_sets* out) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!dev_buf || !out) return RELAXKV_EINVAL;
+    if (((uintptr_t)dev_buf) % kAlign) return RELAXKV_EINVAL;
+    const int32_t k = relaxkv_anchor_count(p->anchor_ratio, p->T_c);
+    SetsLayout l = sets_layout(p, k);
+    if (bytes < l.total) return RELAXKV_ENOSPACE;
+    char* b = (char*)dev_buf;
+    relaxkv_sets s;
+    s.L = p->L;
+    s.T_c = p->T_c;
+    s.k = k;
+    s.anchors = (int32_t*)b; b += l.anchors;
+    s.h = (int32_t*)b; b += l.h;
+    s.U = (int32_t*)b; b += l.U;
+    s.cidx = (int32_t*)b; b += l.cidx;
+    s.R_off = (int32_t*)b; b += l.R_off;
+    s.R_idx = (int32_t*)b; b += l.R_idx;
+    s.R_u = (int32_t*)b; b += l.R_u;
+    s.src = (int32_t*)b; b += l.src;
+    s.counts = (int32_t*)b; b += l.counts;
+    s.edges = (int64_t*)b;
+    *out = s;
+    return RELAXKV_OK;
+}
+
+relaxkv_status relaxkv_score(const relaxkv_problem* p, void* ws, size_t ws_bytes,
+                             float* scores, void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!ws || !scores) return RELAXKV_EINVAL;
+    ScoreWorkspace w = score_workspace_layout(*p);
+    if (ws_bytes < w.total) return RELAXKV_ENOSPACE;
+    return from_hip(launch_score(*p, w, (char*)ws, scores, (hipStream_t)stream));
+}
+
+relaxkv_status relaxkv_select(const relaxkv_problem* p, const float* scores,
+                              const relaxkv_sets* s, void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!scores || !sets_match(p, s)) return RELAXKV_EINVAL;
+    return from_hip(launch_select(*p, scores, *s, (hipStream_t)stream));
+}
+
+relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, const relaxkv_sets* s,
+                                  void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!sets_match(p, s)) return RELAXKV_EINVAL;
+    return from_hip(launch_build_sets(*p, *s, (hipStream_t)stream));
+}
+
+relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets* s,
+                                   int32_t layer, const void* q_new, const void* k_new,
+                                   const void* v_new, void* out, float* lse_out,
+                                   int32_t context_mode, void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!sets_match(p, s)) return RELAXKV_EINVAL;
+    if (layer < 0 || layer >= p->L) return RELAXKV_EINVAL;
+    if (!q_new || !k_new || !v_new || !out) return RELAXKV_EINVAL;
+    if (context_mode != RELAXKV_CONTEXT_UNION && context_mode != RELAXKV_CONTEXT_FULL)
+        return RELAXKV_EINVAL;
+    return from_hip(launch_sparse_attn(*p, *s, layer, q_new, k_new, v_new, out, lse_out,
+                                       context_mode, (hipStream_t)stream));
+}
+
+relaxkv_status relaxkv_counts_to_host(const relaxkv_sets* s, int32_t* host_counts,
+                                      int64_t* host_edges, void* stream) {
+    if (!s || !s->counts || !s->edges || !host_counts || s->L < 1) return RELAXKV_EINVAL;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = hipMemcpyAsync(host_counts, s->counts, sizeof(int32_t) * (s->L + 2),
+                                  hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess && host_edges)
+        e = hipMemcpyAsync(host_edges, s->edges, sizeof(int64_t) * 2 * s->L,
+                           hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return RELAXKV_EDEVICE;
+    return host_counts[s->L + 1] != 0 ? RELAXKV_EINVAL : RELAXKV_OK;
+}
+
+}  // extern "C"

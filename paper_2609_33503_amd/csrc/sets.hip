@@ -1,0 +1,182 @@
+// Repair schedule and compact context (Sec. 3.2 set equations, App. A.1-A.2):
+//   h_i = max{l : i in S_l},  U = union_l S_l (sorted),  R_l = {i in U : h_i >= l},
+// the compact index of every union position, the per-layer source map
+// (rank within R_l, or -1 for a cached row), the CSR lists of R_l and the
+// edge counts sum_{p in R_l} |C_l(p)| and sum_{p in R_l} (p + 1).
+//
+// Four launches: reset h; integer atomicMax of each anchor's layer into h;
+// one workgroup that compacts U in position order and counts |R_l| from the
+// histogram of h; one workgroup per layer that compacts R_l out of U.  All
+// compactions are block prefix scans, so every output is deterministic.
+
+#include "dev_common.h"
+#include "internal.h"
+
+namespace relaxkv {
+namespace {
+
+constexpr int kSetThreads = 1024;
+constexpr int kSetPerThread = 8;
+
+__global__ void sets_reset(int32_t* __restrict__ h, int T) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < T; i += gridDim.x * blockDim.x)
+        h[i] = -1;
+}
+
+__global__ void sets_mark(const int32_t* __restrict__ anchors, int L, int k, int T,
+                          int32_t* __restrict__ h) {
+    const long n = (long)L * k;
+    for (long j = blockIdx.x * (long)blockDim.x + threadIdx.x; j < n;
+         j += (long)gridDim.x * blockDim.x) {
+        const int pos = anchors[j];
+        if (pos >= 0 && pos < T) atomicMax(&h[pos], (int)(j / k));
+    }
+}
+
+// Single workgroup: U, cidx, |U|, |R_l| and R_off.
+__global__ __launch_bounds__(kSetThreads) void sets_union(const int32_t* __restrict__ h, int T,
+                                                          int L, int32_t* __restrict__ U,
+                                                          int32_t* __restrict__ cidx,
+                                                          int32_t* __restrict__ R_off,
+                                                          int32_t* __restrict__ counts) {
+    __shared__ int hist[RELAXKV_MAX_LAYERS];
+    __shared__ int scan_scratch[kSetThreads / 64];
+    const int tid = threadIdx.x;
+    for (int l = tid; l < L; l += kSetThreads) hist[l] = 0;
+    __syncthreads();
+
+    int c_base = 0;
+    for (int base = 0; base < T; base += kSetThreads * kSetPerThread) {
+        const int i0 = base + tid * kSetPerThread;
+        int hv[kSetPerThread];
+        int n = 0;
+#pragma unroll
+        for (int e = 0; e < kSetPerThread; ++e) {
+            const int i = i0 + e;
+            hv[e] = i < T ? h[i] : -1;
+            n += hv[e] >= 0;
+        }
+        int tot;
+        int c = block_exclusive_scan<kSetThreads>(n, scan_scratch, tot) + c_base;
+#pragma unroll
+        for (int e = 0; e < kSetPerThread; ++e) {
+            const int i = i0 + e;
+            if (i >= T) break;
+            if (hv[e] >= 0) {
+                U[c] = i;
+                cidx[i] = c;
+                ++c;
+                atomicAdd(&hist[hv[e]], 1);
+            } else {
+                cidx[i] = -1;
+            }
+        }
+        c_base += tot;
+    }
+    __syncthreads();
+
+    // |R_l| = #{i : h_i >= l}: suffix sums of the histogram, then R_off is the
+    // exclusive prefix of |R_l| over layers.  L <= 1024 = one layer per thread.
+    const int rl = tid < L ? hist[L - 1 - tid] : 0;
+    int tot1;
+    const int sfx = block_exclusive_scan<kSetThreads>(rl, scan_scratch, tot1) + rl;  // layer L-1-tid
+    __syncthreads();
+    if (tid < L) hist[L - 1 - tid] = sfx;     // hist[l] now holds |R_l|
+    __syncthreads();
+    const int nr = tid < L ? hist[tid] : 0;
+    int tot2;
+    const int off = block_exclusive_scan<kSetThreads>(nr, scan_scratch, tot2);
+    if (tid < L) {
+        R_off[tid] = off;
+        counts[1 + tid] = nr;
+    }
+    if (tid == 0) {
+        R_off[L] = tot2;
+        counts[0] = c_base;
+    }
+}
+
+// One workgroup per layer: R_l in position order, its compact indices, the
+// source map and the edge counts.
+__global__ __launch_bounds__(kSetThreads) void sets_layers(
+    const int32_t* __restrict__ h, const int32_t* __restrict__ U, int T,
+    const int32_t* __restrict__ R_off, const int32_t* __restrict__ counts,
+    int32_t* __restrict__ R_idx, int32_t* __restrict__ R_u, int32_t* __restrict__ src,
+    int64_t* __restrict__ edges, int L) {
+    __shared__ int scan_scratch[kSetThreads / 64];
+    __shared__ long long red[2][kSetThreads / 64];
+    const int l = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int nU = counts[0];
+    const int off = R_off[l];
+    int32_t* src_l = src + (size_t)l * T;
+    long long e_sum = 0, ef_sum = 0;
+    int r_base = 0;
+    for (int base = 0; base < nU; base += kSetThreads * kSetPerThread) {
+        const int c0 = base + tid * kSetPerThread;
+        int pos[kSetPerThread];
+        bool act[kSetPerThread];
+        int n = 0;
+#pragma unroll
+        for (int e = 0; e < kSetPerThread; ++e) {
+            const int c = c0 + e;
+            pos[e] = c < nU ? U[c] : 0;
+            act[e] = c < nU && h[pos[e]] >= l;
+            n += act[e];
+        }
+        int tot;
+        int r = block_exclusive_scan<kSetThreads>(n, scan_scratch, tot) + r_base;
+#pragma unroll
+        for (int e = 0; e < kSetPerThread; ++e) {
+            const int c = c0 + e;
+            if (c >= nU) break;
+            if (act[e]) {
+                R_idx[off + r] = pos[e];
+                R_u[off + r] = c;
+                src_l[c] = r;
+                ++r;
+                e_sum += c + 1;          // |C_l(p)| = compact index of p + 1
+                ef_sum += pos[e] + 1;    // full causal prefix
+            } else {
+                src_l[c] = -1;
+            }
+        }
+        r_base += tot;
+    }
+    e_sum = wave_sum(e_sum);
+    ef_sum = wave_sum(ef_sum);
+    const int lane = tid & 63, w = tid >> 6;
+    if (lane == 0) {
+        red[0][w] = e_sum;
+        red[1][w] = ef_sum;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        long long a = 0, b = 0;
+        for (int i = 0; i < kSetThreads / 64; ++i) {
+            a += red[0][i];
+            b += red[1][i];
+        }
+        edges[l] = a;
+        edges[L + l] = b;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s, hipStream_t st) {
+    const int T = p.T_c, L = p.L;
+    const int rb = (T + 255) / 256;
+    hipLaunchKernelGGL(sets_reset, dim3(rb < 1024 ? rb : 1024), dim3(256), 0, st, s.h, T);
+    const long nm = (long)L * s.k;
+    const long mb = (nm + 255) / 256;
+    hipLaunchKernelGGL(sets_mark, dim3(mb < 2048 ? (int)mb : 2048), dim3(256), 0, st, s.anchors,
+                       L, s.k, T, s.h);
+    hipLaunchKernelGGL(sets_union, dim3(1), dim3(kSetThreads), 0, st, s.h, T, L, s.U, s.cidx,
+                       s.R_off, s.counts);
+    hipLaunchKernelGGL(sets_layers, dim3(L), dim3(kSetThreads), 0, st, s.h, s.U, T, s.R_off,
+                       s.counts, s.R_idx, s.R_u, s.src, s.edges, L);
+    return hipGetLastError();
+}
+
+}  // namespace relaxkv

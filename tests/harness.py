@@ -1,0 +1,136 @@
+"""Shared helpers for the GPU parity tests: run the library and the oracle on
+the same seeded inputs and compare them.  Inputs are generated on the device by
+``paper_2609_33503_amd.synth`` and copied to the host for the oracle; no oracle
+input or expected value comes out of the HIP library."""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2609_33503_amd import relaxkv, synth
+
+
+def fp_tol(w):
+    """(kind, value): bf16 inputs compare max-abs within 2e-2; fp32 inputs
+    compare tensor-relative max|x - y| <= 1e-5 max|y|."""
+    return ("abs", 2e-2) if w.dtype == "bf16" else ("rel", 1e-5)
+
+
+def assert_close(got, ref, w, what, rel_gate=None):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), what
+    err = float(np.max(np.abs(got - ref))) if got.size else 0.0
+    scale = float(np.max(np.abs(ref))) if ref.size else 0.0
+    kind, tol = fp_tol(w)
+    if kind == "abs":
+        assert err <= tol, f"{what}: max-abs {err:.3e} > {tol}"
+    else:
+        assert err <= tol * max(scale, 1e-30), f"{what}: rel {err / max(scale, 1e-30):.3e} > {tol}"
+    if rel_gate is not None and scale > 0:
+        assert err / scale <= rel_gate, f"{what}: normalised {err / scale:.3e} > {rel_gate}"
+    return err, scale
+
+
+class Case:
+    """Device inputs of one workload plus the bound library request."""
+
+    def __init__(self, w, q_lse=None, ratio=None, layers=None):
+        self.w = w
+        dev = "cuda"
+        self.q, self.kc, self.vc = synth.make_cache(w, dev, layers=layers)
+        self.ratio = w.ratio if ratio is None else ratio
+        self.req = relaxkv.Request(self.q, self.kc, self.vc, self.ratio, q_lse=q_lse)
+        self.L = self.q.shape[0]
+        self.T = w.T_c
+        self.k = self.req.k
+        self.sets = self.req.alloc_sets()
+        self.ws = self.req.alloc_workspace()
+
+    # ---------------------------------------------------------------- GPU
+    def gpu_scores(self):
+        a = torch.empty(self.L, self.T, dtype=torch.float32, device="cuda")
+        self.req.score(self.ws, a)
+        torch.cuda.synchronize()
+        return a
+
+    def gpu_select(self, scores_f32):
+        self.req.select(scores_f32, self.sets)
+        torch.cuda.synchronize()
+        return self.sets.anchors.cpu().numpy().astype(np.int64)
+
+    def gpu_sets(self):
+        self.req.build_sets(self.sets)
+        counts, edges = self.sets.counts_to_host()
+        L, T = self.L, self.T
+        nU = counts[0]
+        R_off = self.sets.R_off.cpu().numpy()
+        R_idx = self.sets.R_idx.cpu().numpy()
+        R_u = self.sets.R_u.cpu().numpy()
+        src = self.sets.src.cpu().numpy()
+        return dict(
+            counts=counts, edges=edges, h=self.sets.h.cpu().numpy(),
+            U=self.sets.U.cpu().numpy()[:nU], cidx=self.sets.cidx.cpu().numpy(),
+            R_off=R_off,
+            R=[R_idx[R_off[l]:R_off[l + 1]] for l in range(L)],
+            R_u=[R_u[R_off[l]:R_off[l + 1]] for l in range(L)],
+            src=[src[l, :nU] for l in range(L)])
+
+    def fresh(self, layer, R_l):
+        """Compact fresh rows of the targets R_l of one layer (device tensors)."""
+        qn, kn, vn = synth.make_fresh_layer(self.w, layer, self.kc[layer], self.vc[layer], "cuda")
+        return (synth.gather_rows(qn, R_l), synth.gather_rows(kn, R_l),
+                synth.gather_rows(vn, R_l))
+
+    def gpu_attn(self, layer, fresh, n_R, mode=relaxkv.CONTEXT_UNION):
+        qn, kn, vn = fresh
+        out = torch.empty(n_R, self.w.H, self.w.d, dtype=self.q.dtype, device="cuda")
+        lse = torch.empty(n_R, self.w.H, dtype=torch.float32, device="cuda")
+        self.req.sparse_attn(self.sets, layer, qn, kn, vn, out, lse, context_mode=mode)
+        torch.cuda.synchronize()
+        return out, lse
+
+    # ---------------------------------------------------------------- oracle
+    def oracle_scores(self, layers=None):
+        layers = range(self.L) if layers is None else layers
+        q = synth.to_f64(self.q[list(layers)])
+        k = synth.to_f64(self.kc[list(layers)])
+        return oracle.score(q, k)
+
+    def oracle_attn(self, layer, sets, fresh, mode="union", targets=None):
+        qn, kn, vn = (synth.to_f64(t) for t in fresh)
+        return oracle.sparse_attn(layer, sets, qn, kn, vn, synth.to_f64(self.kc[layer]),
+                                  synth.to_f64(self.vc[layer]), mode=mode, targets=targets)
+
+
+def compare_sets(got, ref):
+    """Bit-exact comparison of the GPU sets with the oracle's."""
+    L = len(ref.R)
+    assert got["h"].tolist() == ref.h.tolist()
+    assert got["U"].tolist() == ref.U.tolist()
+    assert got["cidx"].tolist() == ref.cidx.tolist()
+    assert got["counts"][0] == len(ref.U)
+    for l in range(L):
+        assert got["counts"][1 + l] == len(ref.R[l]), l
+        assert got["R"][l].tolist() == ref.R[l].tolist(), l
+        assert got["R_u"][l].tolist() == ref.R_u[l].tolist(), l
+        assert got["src"][l].tolist() == ref.src[l].tolist(), l
+        assert got["edges"][l] == int(ref.edges[l]), l
+        assert got["edges"][L + l] == int(ref.edges_full[l]), l
+    assert got["counts"][L + 1] == 0
+
+
+def synthetic_scores(L, T, seed, levels=None):
+    """Seeded score matrix in [0, 1] with many exact ties and signed zeros
+    (used to drive selection and set building at full size independently of
+    any scoring)."""
+    rng = np.random.default_rng(seed)
+    a = rng.random((L, T), dtype=np.float32)
+    if levels:
+        a = (np.floor(a * levels) / levels).astype(np.float32)
+    z = rng.random((L, T)) < 0.05
+    a[z] = np.where(rng.random(int(z.sum())) < 0.5, np.float32(-0.0), np.float32(0.0))
+    return a

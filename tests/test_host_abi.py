@@ -1,0 +1,181 @@
+"""Host-side checks of the C ABI (no GPU): the library loads and exports every
+symbol include/relaxkv.h declares; argument validation, anchor budget, and
+buffer sizing/carving behave as documented.  No call here reaches a kernel:
+every call either fails validation before anything is enqueued or is a
+host-only function."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from oracle import anchor_count as oracle_anchor_count
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "relaxkv.h")
+
+
+@pytest.fixture(scope="module")
+def rk():
+    from paper_2609_33503_amd import build, relaxkv
+    if not os.path.exists(relaxkv._LIB_PATH):
+        build.build()
+    relaxkv.load()
+    return relaxkv
+
+
+def _declared():
+    txt = open(HEADER).read()
+    decl = r"^(?:const char\*|int32_t|size_t|relaxkv_status)\s+(relaxkv_[a-z_]+)\("
+    return sorted(set(re.findall(decl, txt, re.M)))
+
+
+def test_exports_match_header(rk):
+    declared = _declared()
+    assert set(declared) == set(rk.EXPORTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", rk._LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (relaxkv_[a-z_]+)$", out, re.M))
+    assert exported == set(declared)
+    lib = rk.load()
+    for name in declared:
+        assert hasattr(lib, name)
+
+
+def test_status_strings(rk):
+    lib = rk.load()
+    for s in (0, -1, -2, -3, -4):
+        assert lib.relaxkv_status_string(s).decode()
+    assert lib.relaxkv_status_string(12345) == b"unknown status"
+
+
+@pytest.mark.parametrize("r,T", [(0.15, 1024), (0.15, 8192), (0.05, 16384), (0.15, 16384),
+                                 (0.30, 16384), (0.15, 32768), (0.125, 20), (0.375, 4),
+                                 (0.625, 4), (0.5, 1), (0.0, 50), (1.0, 77), (0.5, 3),
+                                 (0.3, 5), (1e-9, 10), (0.999999, 1000)])
+def test_anchor_count_matches_oracle(rk, r, T):
+    assert rk.load().relaxkv_anchor_count(r, T) == oracle_anchor_count(r, T)
+
+
+@pytest.mark.parametrize("r,T", [(-0.1, 10), (1.5, 10), (float("nan"), 10), (float("inf"), 10),
+                                 (0.2, 0), (0.2, -5)])
+def test_anchor_count_rejects(rk, r, T):
+    assert rk.load().relaxkv_anchor_count(r, T) == rk.EINVAL
+
+
+def _problem(rk, **kw):
+    base = dict(L=4, T_c=2048, n_query=16, H=8, H_kv=2, d=128, dtype=rk.DTYPE_BF16,
+                softmax_scale=0.0, anchor_ratio=0.15, q=0x1000, k_cache=0x2000, v_cache=0x3000,
+                q_lse=None)
+    base.update(kw)
+    return rk.Problem(base["L"], base["T_c"], base["n_query"], base["H"], base["H_kv"],
+                      base["d"], base["dtype"], base["softmax_scale"], base["anchor_ratio"],
+                      base["q"], base["k_cache"], base["v_cache"], base["q_lse"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({}, 0),
+    ({"L": 0}, -1), ({"T_c": 0}, -1), ({"n_query": 0}, -1), ({"H": 6, "H_kv": 4}, -1),
+    ({"H_kv": 0}, -1), ({"L": 1025}, -1), ({"T_c": (1 << 22) + 1}, -1),
+    ({"q": None}, -1), ({"k_cache": None}, -1), ({"v_cache": None}, -1),
+    ({"anchor_ratio": -0.5}, -1), ({"anchor_ratio": float("nan")}, -1),
+    ({"softmax_scale": float("nan")}, -1), ({"softmax_scale": float("inf")}, -1),
+    ({"d": 96}, -3), ({"d": 256}, -3), ({"dtype": 7}, -3),
+    ({"H": 256, "H_kv": 1}, -3),                      # a GQA group wider than the bf16 tile
+    ({"H": 256, "H_kv": 1, "dtype": 0}, 0),           # fp32 kernels have no such limit
+    ({"d": 64, "dtype": 0}, 0),
+])
+def test_validate(rk, kw, status):
+    p = _problem(rk, **kw)
+    assert rk.load().relaxkv_validate(ctypes.byref(p)) == status
+
+
+def test_validate_null(rk):
+    assert rk.load().relaxkv_validate(None) == rk.EINVAL
+
+
+def test_sizes(rk):
+    lib = rk.load()
+    p = _problem(rk)
+    ws = lib.relaxkv_score_workspace_bytes(ctypes.byref(p))
+    sb = lib.relaxkv_sets_bytes(ctypes.byref(p))
+    L, T, k = 4, 2048, oracle_anchor_count(0.15, 2048)
+    assert ws >= L * 2 * T * 4                      # per-KV-head partial sums
+    assert sb >= 4 * (L * k + 3 * T + (L + 1) + 3 * L * T + (L + 2)) + 8 * 2 * L
+    assert sb % 256 == 0 and ws % 256 == 0
+    bad = _problem(rk, d=96)
+    assert lib.relaxkv_score_workspace_bytes(ctypes.byref(bad)) == 0
+    assert lib.relaxkv_sets_bytes(ctypes.byref(bad)) == 0
+
+
+def test_sets_bind_carves_buffer(rk):
+    lib = rk.load()
+    p = _problem(rk)
+    nbytes = lib.relaxkv_sets_bytes(ctypes.byref(p))
+    base = 0x7f0000000000                            # never dereferenced: host-only arithmetic
+    s = rk.Sets()
+    assert lib.relaxkv_sets_bind(ctypes.byref(p), ctypes.c_void_p(base), nbytes,
+                                 ctypes.byref(s)) == 0
+    assert (s.L, s.T_c, s.k) == (4, 2048, oracle_anchor_count(0.15, 2048))
+    ptrs = [s.anchors, s.h, s.U, s.cidx, s.R_off, s.R_idx, s.R_u, s.src, s.counts, s.edges]
+    assert ptrs[0] == base and ptrs == sorted(ptrs)
+    assert all(x % 256 == 0 for x in ptrs)
+    L, T, k = s.L, s.T_c, s.k
+    sizes = [L * k * 4, T * 4, T * 4, T * 4, (L + 1) * 4, L * T * 4, L * T * 4, L * T * 4,
+             (L + 2) * 4, 2 * L * 8]
+    for a, b, n in zip(ptrs, ptrs[1:] + [base + nbytes], sizes):
+        assert b - a >= n
+    assert lib.relaxkv_sets_bind(ctypes.byref(p), ctypes.c_void_p(base), nbytes - 1,
+                                 ctypes.byref(s)) == rk.ENOSPACE
+    assert lib.relaxkv_sets_bind(ctypes.byref(p), ctypes.c_void_p(base + 4), nbytes,
+                                 ctypes.byref(s)) == rk.EINVAL
+    assert lib.relaxkv_sets_bind(ctypes.byref(p), None, nbytes, ctypes.byref(s)) == rk.EINVAL
+
+
+def _bound_sets(rk, p):
+    lib = rk.load()
+    s = rk.Sets()
+    nbytes = lib.relaxkv_sets_bytes(ctypes.byref(p))
+    assert lib.relaxkv_sets_bind(ctypes.byref(p), ctypes.c_void_p(0x7f0000000000), nbytes,
+                                 ctypes.byref(s)) == 0
+    return s
+
+
+def test_compute_calls_reject_before_launch(rk):
+    lib = rk.load()
+    p = _problem(rk)
+    s = _bound_sets(rk, p)
+    fake = ctypes.c_void_p(0x7e0000000000)
+    ws = lib.relaxkv_score_workspace_bytes(ctypes.byref(p))
+    bp = _problem(rk, H=6, H_kv=4)
+    # score
+    assert lib.relaxkv_score(ctypes.byref(p), None, ws, fake, None) == rk.EINVAL
+    assert lib.relaxkv_score(ctypes.byref(p), fake, ws, None, None) == rk.EINVAL
+    assert lib.relaxkv_score(ctypes.byref(p), fake, ws - 1, fake, None) == rk.ENOSPACE
+    assert lib.relaxkv_score(ctypes.byref(bp), fake, ws, fake, None) == rk.EINVAL
+    # select / build_sets: sets bound for another problem are refused
+    other = _problem(rk, T_c=4096)
+    assert lib.relaxkv_select(ctypes.byref(other), fake, ctypes.byref(s), None) == rk.EINVAL
+    assert lib.relaxkv_select(ctypes.byref(p), None, ctypes.byref(s), None) == rk.EINVAL
+    assert lib.relaxkv_select(ctypes.byref(p), fake, None, None) == rk.EINVAL
+    assert lib.relaxkv_build_sets(ctypes.byref(other), ctypes.byref(s), None) == rk.EINVAL
+    s2 = _bound_sets(rk, p)
+    s2.src = None
+    assert lib.relaxkv_build_sets(ctypes.byref(p), ctypes.byref(s2), None) == rk.EINVAL
+    # sparse_attn
+    args = (fake, fake, fake, fake, None)
+    for layer in (-1, 4):
+        assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s), layer, *args, 0,
+                                       None) == rk.EINVAL
+    assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s), 0, *args, 2,
+                                   None) == rk.EINVAL
+    assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s), 0, None, fake, fake, fake,
+                                   None, 0, None) == rk.EINVAL
+    assert lib.relaxkv_sparse_attn(ctypes.byref(_problem(rk, d=96)), ctypes.byref(s), 0, *args,
+                                   0, None) == rk.EUNSUPPORTED
+    # counts_to_host
+    c = (ctypes.c_int32 * 6)()
+    assert lib.relaxkv_counts_to_host(None, c, None, None) == rk.EINVAL
+    assert lib.relaxkv_counts_to_host(ctypes.byref(s), None, None, None) == rk.EINVAL
