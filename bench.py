@@ -21,6 +21,7 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -38,6 +39,27 @@ from paper_2609_33503_amd import relaxkv, synth  # noqa: E402
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_qwen14b-32k-planted.traffic.json")
+KERNEL_SOURCES = ("paper_2609_33503_amd/csrc/attn.hip", "paper_2609_33503_amd/csrc/internal.h",
+                  "paper_2609_33503_amd/csrc/dev_common.h")
+
+
+def measured_traffic(workload):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE scaled by a 1 GiB copy), or None when the
+    kernel sources changed since the counters were taken or the workload differs."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except OSError:
+        return None
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    if t.get("source_sha256") != h.hexdigest() or t.get("workload") != workload:
+        return None
+    return float(t["traffic_bytes_per_launch"])
 
 
 def log(*a):
@@ -165,6 +187,9 @@ def main():
     ap.add_argument("--control", action="store_true",
                     help="also time the Full-Prefix Control on the same targets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run one plain device-to-device copy of MIB MiB (reference "
+                         "kernel for scaling the HBM byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the hot path is benchmarked on a single "
@@ -173,6 +198,15 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n}))
+        return
     relaxkv.load()
     w = synth.WORKLOADS[args.workload]
     b = Bench(w)
@@ -212,7 +246,8 @@ def main():
                  "edges": E, "edges_full_prefix": E_full,
                  "flop_reduction_vs_full_prefix": 1.0 - E / E_full},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": peak,
-                     "unit": "TFLOP/s", "frac": attn_tflops / peak, "traffic": None,
+                     "unit": "TFLOP/s", "frac": attn_tflops / peak,
+                     "traffic": measured_traffic(w.name),
                      "kernel": "attn_bf16 (relaxkv_sparse_attn)",
                      "avg_launch_ms": r["attn_launch_ms_avg"]},
     }

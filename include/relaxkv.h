@@ -100,6 +100,8 @@ typedef struct relaxkv_problem {
  *   R_u      [L*T_c]       compact index (in U) of each R_idx entry.
  *   src      [L][T_c]      src[l*T_c + c] = rank of U[c] within R_l (its row in the
  *                          fresh K/V of layer l), or -1 (cached row), c < |U|.
+ *   rank     [L][T_c]      rank[l*T_c + j] = rank of position j within R_l, or -1 when j is
+ *                          not an active target of layer l (position-indexed view of src).
  *   counts   [L+2]         counts[0] = |U|; counts[1+l] = |R_l|; counts[L+1] = error
  *                          word (nonzero when a NaN score reached relaxkv_select).
  *   edges    [2L]          edges[l] = sum_{p in R_l} |C_l(p)| (App. A.2 edge count);
@@ -116,6 +118,7 @@ typedef struct relaxkv_sets {
     int32_t* R_idx;
     int32_t* R_u;
     int32_t* src;
+    int32_t* rank;
     int32_t* counts;
     int64_t* edges;
 } relaxkv_sets;

@@ -45,6 +45,7 @@ struct AttnArgs {
     const int32_t* U;
     const int32_t* cidx;
     const int32_t* src_l;    // src + layer * T
+    const int32_t* rank_l;   // rank + layer * T
     const int32_t* R_off;
     const int32_t* R_idx;
     const int32_t* R_u;
@@ -62,8 +63,7 @@ __device__ __forceinline__ size_t kv_row(const AttnArgs& a, int c, int g, bool& 
     int pos, r;
     if (FULL) {
         pos = c;
-        const int ci = a.cidx[c];
-        r = ci >= 0 ? a.src_l[ci] : -1;
+        r = a.rank_l[c];
     } else {
         pos = a.U[c];
         r = a.src_l[c];
@@ -74,18 +74,37 @@ __device__ __forceinline__ size_t kv_row(const AttnArgs& a, int c, int g, bool& 
 
 // ----------------------------------------------------------------- bf16 MFMA
 
-constexpr int BN = kAttnKeys;              // 64 keys per tile
+constexpr float kRescaleSlack = 8.0f;      // log2 units the running max may lag the true max
 
-template <int D, bool FULL>
-__global__ __launch_bounds__(256, 2) void attn_bf16(AttnArgs a) {
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// max / sum of a value and its copy in the lane 32 away (one VALU swap).
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// NW waves x RB*32 rows per workgroup; LDS tiles of BN keys, computed in
+// 64-key steps of two 32-key MFMA blocks.  With RB = 2 every K and V fragment
+// read from LDS feeds two MFMAs (one per 32-row block).
+template <int D, bool FULL, int NW, int BN, int RB>
+__global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(AttnArgs a) {
+    constexpr int NT = NW * 64;            // threads
     constexpr int KS = D / 16;             // k-steps of the QK^T contraction
     constexpr int DB = D / 32;             // 32-wide d blocks of O^T
     constexpr int KSTR = D + 8;            // K tile row stride (elements)
-    constexpr int VSTR = BN + 4;           // V^T tile row stride (elements)
+    constexpr int VSTR = D + 16;           // V tile row stride (elements): rows 8 banks apart
     constexpr int P = D / 8;               // 16-byte parts per row
-    constexpr int KPT = BN * P / 256;      // keys per thread in the loader (4 or 2)
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[BN * KSTR];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VSTR];
+    constexpr int KPT = BN * P / NT;       // keys per thread in the loader
+    static_assert(KPT >= 1 && BN * P == KPT * NT, "loader shape");
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BN * KSTR];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][BN * VSTR];
 
     const int Hkv = a.Hkv;
     const int g = blockIdx.x % Hkv;
@@ -103,156 +122,227 @@ __global__ __launch_bounds__(256, 2) void attn_bf16(AttnArgs a) {
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r32 = lane & 31, hf = lane >> 5;
-    const int rho = w * 32 + r32;                    // this lane's (target, head) row
-    const int tl = rho / a.G, hh = rho - tl * a.G;
-    const int t = t0 + tl;
-    const bool valid = tl < a.BT && t < t1;
-    const int lim = valid ? lim_of[t] : cmax;        // padding rows: finite, never stored
-    const int head = g * a.G + hh;
-
     const uint16_t* qn = (const uint16_t*)a.q_new;
-    bf16x8 qf[KS];
-    {
-        const uint16_t* qrow = qn + ((size_t)(valid ? t : t0) * a.H + (valid ? head : 0)) * D;
+    const float sl2 = a.scale * kLog2e;              // > 0
+
+    // This lane's (target, head) rows, one per 32-row block.
+    int t_of[RB], head_of[RB], lim[RB];
+    bool valid[RB];
+    bf16x8 qf[RB][KS];
+    f32x16 o[RB][DB];
+    float m_run[RB], l_run[RB];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
+    for (int rb = 0; rb < RB; ++rb) {
+        const int rho = (w * RB + rb) * 32 + r32;
+        const int tl = rho / a.G, hh = rho - tl * a.G;
+        t_of[rb] = t0 + tl;
+        valid[rb] = tl < a.BT && t_of[rb] < t1;
+        lim[rb] = valid[rb] ? lim_of[t_of[rb]] : cmax;   // padding rows: finite, never stored
+        head_of[rb] = g * a.G + hh;
+        const uint16_t* qrow =
+            qn + ((size_t)(valid[rb] ? t_of[rb] : t0) * a.H + (valid[rb] ? head_of[rb] : 0)) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qf[rb][ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[rb][db] = f32x16{};
+        m_run[rb] = -INFINITY;
+        l_run[rb] = 0.f;
     }
-    const float sl2 = a.scale * kLog2e;
 
-    f32x16 o[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[db] = f32x16{};
-    float m_run = -INFINITY, l_run = 0.f;
-
-    // loader: thread -> (key group kq, 16-byte part) ; keys kq*KPT .. kq*KPT+KPT-1
+    // Loader: thread -> (key group kq, 16-byte part); keys kq*KPT .. kq*KPT+KPT-1.
+    // Two-stage pipeline: the row indices of tile kt+2 are loaded while tile kt
+    // is computed; the K/V rows of tile kt+1 are loaded from them one step later.
     const int kq = tid / P, part = tid % P;
     const uint16_t* kn = (const uint16_t*)a.k_new;
     const uint16_t* vn = (const uint16_t*)a.v_new;
     const uint16_t* kc = (const uint16_t*)a.kc;
     const uint16_t* vc = (const uint16_t*)a.vc;
+    const int32_t* srcmap = FULL ? a.rank_l : a.src_l;
+    // Per-workgroup bases of KV head g; per key only a row offset is added.
+    const uint16_t* kng = kn + (size_t)g * D;                    // fresh rows: stride Hkv*D
+    const uint16_t* kcg = kc + (size_t)g * a.T * D;              // cached rows: stride D
+    const long dv_fresh = vn - kn;                               // V address = K address + delta
+    const long dv_cached = vc - kc;
+    int ipos[KPT], irow[KPT];                        // position, fresh rank (-1: cached row)
     u32x4 kr[KPT], vr[KPT];
 
-    auto load_tile = [&](int c0) {
+    // Keys past cmax re-read the row of cmax: their logits are masked (every
+    // 64-key step that holds such a key is a staircase step), so only
+    // finiteness matters.
+    auto load_idx = [&](int c0) {
 #pragma unroll
         for (int kk = 0; kk < KPT; ++kk) {
-            const int c = c0 + kq * KPT + kk;
-            if (c <= cmax) {
-                bool fresh;
-                const size_t row = kv_row<FULL>(a, c, g, fresh);
-                const uint16_t* kb = fresh ? kn : kc;
-                const uint16_t* vb = fresh ? vn : vc;
-                kr[kk] = *(const u32x4*)(kb + row * D + part * 8);
-                vr[kk] = *(const u32x4*)(vb + row * D + part * 8);
-            } else {
-                kr[kk] = u32x4{0u, 0u, 0u, 0u};
-                vr[kk] = u32x4{0u, 0u, 0u, 0u};
-            }
+            const int c = min(c0 + kq * KPT + kk, cmax);
+            ipos[kk] = FULL ? c : a.U[c];
+            irow[kk] = srcmap[c];
+        }
+    };
+    auto load_rows = [&]() {
+#pragma unroll
+        for (int kk = 0; kk < KPT; ++kk) {
+            const bool fresh = irow[kk] >= 0;
+            const uint16_t* kp = fresh ? kng + (size_t)irow[kk] * (Hkv * D) : kcg + (size_t)ipos[kk] * D;
+            kp += part * 8;
+            kr[kk] = *(const u32x4*)kp;
+            vr[kk] = *(const u32x4*)(kp + (fresh ? dv_fresh : dv_cached));
         }
     };
 
+    // Transposing V reads: lane (group G = lane/16, j = lane%16) points at key row
+    // 4*(G/2) + j/4 and d column (G%2)*16 + 4*(j%4) of each 16-key, 32-d block.
+    // ds_read_b64_tr_b16 gives lane i of a 16-lane group element i%4 of the
+    // 8-byte chunks read by lanes 4m + i/4 (m = 0..3), so lane i receives 4 keys
+    // at one d: element e of the k-index block hf*8 .. hf*8+7 of half k2 is key
+    // 16*k2 + 8(e/4) + 4hf + e%4 of the 32-key block, the S^T lane layout.
+    const int vtr_off = (4 * (lane >> 5) + ((lane & 15) >> 2)) * VSTR + ((lane >> 4) & 1) * 16 +
+                        4 * (lane & 3);
+
     const int nkt = cmax / BN + 1;
-    load_tile(0);
+    load_idx(0);
+    load_rows();
+    if (nkt > 1) load_idx(BN);
     for (int kt = 0; kt < nkt; ++kt) {
-        const int c0 = kt * BN;
-        __syncthreads();                              // previous tile fully consumed
+        uint16_t* ks_b = Ks[kt & 1];
+        uint16_t* vs_b = Vs[kt & 1];
+        // Store tile kt.  The buffer was last read in step kt-2, which every wave
+        // finished before the barrier of step kt-1.
 #pragma unroll
-        for (int kk = 0; kk < KPT; ++kk)
-            *(u32x4*)(Ks + (kq * KPT + kk) * KSTR + part * 8) = kr[kk];
-        // V transposed: Vt[d][key]; this thread holds KPT keys x 8 d values.
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int sh = (e & 1) * 16;
-            const int wd = e >> 1;
-            if constexpr (KPT == 4) {
-                const uint32_t lo = ((vr[0][wd] >> sh) & 0xffffu) | (((vr[1][wd] >> sh) & 0xffffu) << 16);
-                const uint32_t hi = ((vr[2][wd] >> sh) & 0xffffu) | (((vr[3][wd] >> sh) & 0xffffu) << 16);
-                *(u32x2*)(Vt + (part * 8 + e) * VSTR + kq * KPT) = u32x2{lo, hi};
-            } else {
-                const uint32_t lo = ((vr[0][wd] >> sh) & 0xffffu) | (((vr[1][wd] >> sh) & 0xffffu) << 16);
-                *(uint32_t*)(Vt + (part * 8 + e) * VSTR + kq * KPT) = lo;
-            }
+        for (int kk = 0; kk < KPT; ++kk) {
+            *(u32x4*)(ks_b + (kq * KPT + kk) * KSTR + part * 8) = kr[kk];
+            *(u32x4*)(vs_b + (kq * KPT + kk) * VSTR + part * 8) = vr[kk];
         }
         __syncthreads();
-        if (kt + 1 < nkt) load_tile(c0 + BN);
-
-        // S^T = K Q^T for two 32-key blocks
-        f32x16 s0 = {}, s1 = {};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 k0 = *(const bf16x8*)(Ks + r32 * KSTR + ks * 16 + hf * 8);
-            const bf16x8 k1 = *(const bf16x8*)(Ks + (32 + r32) * KSTR + ks * 16 + hf * 8);
-            s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
-            s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], s1, 0, 0, 0);
+        if (kt + 1 < nkt) {
+            load_rows();                                   // tile kt+1
+            if (kt + 2 < nkt) load_idx((kt + 2) * BN);     // indices of tile kt+2
         }
-        // s_kb[v] = S[row][key c0 + kb*32 + 8(v/4) + 4hf + v%4], in log2 units below
-        const bool masked = c0 + BN - 1 > cmin;
-        float mx = -INFINITY;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int kc0 = c0 + 8 * (v >> 2) + 4 * hf + (v & 3);
-            float x0 = s0[v] * sl2, x1 = s1[v] * sl2;
-            if (masked) {
-                if (kc0 > lim) x0 = -INFINITY;
-                if (kc0 + 32 > lim) x1 = -INFINITY;
+        for (int sub = 0; sub < BN / 64; ++sub) {
+            const int c0 = kt * BN + sub * 64;
+            if (c0 > cmax) break;
+            const uint16_t* kst = ks_b + sub * 64 * KSTR;
+            const uint16_t* vst = vs_b + sub * 64 * VSTR;
+            // S^T = K Q^T: s[rb][kb][v] = S[row rb][key c0 + kb*32 + 8(v/4) + 4hf + v%4]
+            f32x16 s[RB][2];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x16{};
+            // K fragments are read two k-steps ahead of the MFMAs that use them.
+            bf16x8 kf[KS][2];
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                kf[ks][0] = *(const bf16x8*)(kst + r32 * KSTR + ks * 16 + hf * 8);
+                kf[ks][1] = *(const bf16x8*)(kst + (32 + r32) * KSTR + ks * 16 + hf * 8);
             }
-            s0[v] = x0;
-            s1[v] = x1;
-            mx = fmaxf(mx, fmaxf(x0, x1));
-        }
-        mx = fmaxf(mx, swap_half(mx));
-        const float m_new = fmaxf(m_run, mx);        // finite: key 0 is in every row's context
-        const float alpha = fast_exp2(m_run - m_new);
-        float ls = 0.f;
-        bf16x8 pb[2][2];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const float p0 = fast_exp2(s0[v] - m_new);
-            const float p1 = fast_exp2(s1[v] - m_new);
-            ls += p0 + p1;
-            pb[0][v >> 3][v & 7] = (__bf16)p0;
-            pb[1][v >> 3][v & 7] = (__bf16)p1;
-        }
-        l_run = l_run * alpha + ls;
-        m_run = m_new;
+            for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[db] *= alpha;
-
-        // O^T += V^T P^T ; k-index hf*8+e of step (kb, k2) is key
-        // kb*32 + k2*16 + 8(e/4) + 4hf + e%4, matching the S^T lane layout.
+                for (int rb = 0; rb < RB; ++rb) {
+                    s[rb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][0], qf[rb][ks], s[rb][0], 0, 0, 0);
+                    s[rb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][1], qf[rb][ks], s[rb][1], 0, 0, 0);
+                }
+            }
+#if RELAXKV_ATTN_SCHED
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // 4 LDS reads
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-            const uint16_t* vrow = Vt + (db * 32 + r32) * VSTR;
+            for (int ks = 0; ks < KS; ++ks) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 2 * RB, 0);
+                if (ks + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            }
+#endif
+            if (c0 + 63 > cmin) {                          // staircase step: mask
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int key = c0 + 8 * (v >> 2) + 4 * hf + (v & 3);
+                        if (key > lim[rb]) s[rb][0][v] = -INFINITY;
+                        if (key + 32 > lim[rb]) s[rb][1][v] = -INFINITY;
+                    }
+            }
+            // Row max over the step in log2 units.  Lazy rescaling: the running
+            // max only moves when the step's max exceeds it by more than
+            // kRescaleSlack, so p <= 2^kRescaleSlack and most steps skip the O
+            // rescale.  Both halves of a row take the same decision.
+            float mx[RB];
+            bool need = false;
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                float m = fmaxf(s[rb][0][0], s[rb][1][0]);
+#pragma unroll
+                for (int v = 1; v < 16; ++v) m = fmaxf(m, fmaxf(s[rb][0][v], s[rb][1][v]));
+                mx[rb] = pair_max(m) * sl2;
+                need |= mx[rb] > m_run[rb] + kRescaleSlack;
+            }
+            if (__any(need)) {
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb) {
+                    const float m_new = mx[rb] > m_run[rb] + kRescaleSlack ? mx[rb] : m_run[rb];
+                    const float alpha = fast_exp2(m_run[rb] - m_new);
+                    l_run[rb] *= alpha;
+#pragma unroll
+                    for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+                    m_run[rb] = m_new;
+                }
+            }
+            // P^T as bf16 B operands: pb[rb][kb][k2] holds values 8*k2 .. 8*k2+7.
+            bf16x8 pb[RB][2][2];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                float ls = 0.f;
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const float p = fast_exp2(fmaf(s[rb][kb][v], sl2, -m_run[rb]));
+                        ls += p;
+                        pb[rb][kb][v >> 3][v & 7] = (__bf16)p;
+                    }
+                l_run[rb] += ls;
+            }
+            // O^T += V^T P^T
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-                for (int k2 = 0; k2 < 2; ++k2) {
-                    const int ko = kb * 32 + k2 * 16 + 4 * hf;
-                    const bf16x4 va = *(const bf16x4*)(vrow + ko);
-                    const bf16x4 vb = *(const bf16x4*)(vrow + ko + 8);
-                    const bf16x8 vv = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
-                    o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pb[kb][k2], o[db], 0, 0, 0);
+                for (int db = 0; db < DB; ++db) {
+#pragma unroll
+                    for (int k2 = 0; k2 < 2; ++k2) {
+                        const uint16_t* p0 = vst + vtr_off + (kb * 32 + k2 * 16) * VSTR + db * 32;
+                        const v4i16 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p0);
+                        const v4i16 a1 =
+                            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 8 * VSTR));
+                        const bf16x8 vv = __builtin_bit_cast(
+                            bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb)
+                            o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pb[rb][kb][k2],
+                                                                                o[rb][db], 0, 0, 0);
+                    }
                 }
             }
         }
     }
 
-    const float l_tot = l_run + swap_half(l_run);
-    if (!valid) return;
-    const float inv = 1.0f / l_tot;
-    uint16_t* out = (uint16_t*)a.out + ((size_t)t * a.H + head) * D;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
+    for (int rb = 0; rb < RB; ++rb) {
+        const float l_tot = pair_sum(l_run[rb]);
+        if (!valid[rb]) continue;
+        const float inv = 1.0f / l_tot;
+        uint16_t* out = (uint16_t*)a.out + ((size_t)t_of[rb] * a.H + head_of[rb]) * D;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int d0 = db * 32 + 8 * j + 4 * hf;
-            const uint32_t lo = (uint32_t)f32_to_bf16_bits(o[db][4 * j] * inv) |
-                                ((uint32_t)f32_to_bf16_bits(o[db][4 * j + 1] * inv) << 16);
-            const uint32_t hi = (uint32_t)f32_to_bf16_bits(o[db][4 * j + 2] * inv) |
-                                ((uint32_t)f32_to_bf16_bits(o[db][4 * j + 3] * inv) << 16);
-            *(u32x2*)(out + d0) = u32x2{lo, hi};
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int d0 = db * 32 + 8 * j + 4 * hf;
+                const uint32_t lo = (uint32_t)f32_to_bf16_bits(o[rb][db][4 * j] * inv) |
+                                    ((uint32_t)f32_to_bf16_bits(o[rb][db][4 * j + 1] * inv) << 16);
+                const uint32_t hi = (uint32_t)f32_to_bf16_bits(o[rb][db][4 * j + 2] * inv) |
+                                    ((uint32_t)f32_to_bf16_bits(o[rb][db][4 * j + 3] * inv) << 16);
+                *(u32x2*)(out + d0) = u32x2{lo, hi};
+            }
         }
+        if (a.lse && hf == 0)
+            a.lse[(size_t)t_of[rb] * a.H + head_of[rb]] = (m_run[rb] + __log2f(l_tot)) * kLn2;
     }
-    if (a.lse && hf == 0) a.lse[(size_t)t * a.H + head] = (m_run + __log2f(l_tot)) * kLn2;
 }
 
 // ----------------------------------------------------------------- fp32 VALU
@@ -314,11 +404,17 @@ __global__ __launch_bounds__(64) void attn_f32(AttnArgs a) {
     if (a.lse && lane == 0) a.lse[(size_t)t * a.H + head] = m_run + logf(l_run);
 }
 
+constexpr int kNW = RELAXKV_ATTN_WAVES;
+constexpr int kBN = RELAXKV_ATTN_TILE;
+constexpr int kRB = RELAXKV_ATTN_ROWBLOCKS;
+static_assert(kAttnRows == kNW * kRB * 32, "rows per workgroup");
+
 template <int D, bool FULL>
 void launch_one(const AttnArgs& a, bool bf16, int n_bound, hipStream_t st) {
     if (bf16) {
         const int ntiles = (n_bound + a.BT - 1) / a.BT;
-        hipLaunchKernelGGL((attn_bf16<D, FULL>), dim3(ntiles * a.Hkv), dim3(256), 0, st, a);
+        hipLaunchKernelGGL((attn_bf16<D, FULL, kNW, kBN, kRB>), dim3(ntiles * a.Hkv), dim3(kNW * 64),
+                           0, st, a);
     } else {
         hipLaunchKernelGGL((attn_f32<D, FULL>), dim3(n_bound, a.H), dim3(64), 0, st, a);
     }
@@ -341,6 +437,7 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.U = s.U;
     a.cidx = s.cidx;
     a.src_l = s.src + (size_t)layer * p.T_c;
+    a.rank_l = s.rank + (size_t)layer * p.T_c;
     a.R_off = s.R_off;
     a.R_idx = s.R_idx;
     a.R_u = s.R_u;
@@ -352,7 +449,7 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.G = p.H / p.H_kv;
     a.T = p.T_c;
     a.layer = layer;
-    a.BT = kAttnRows / a.G;
+    a.BT = bf16 ? kNW * kRB * 32 / a.G : 1;
     a.scale = p.softmax_scale > 0.f ? p.softmax_scale : 1.0f / sqrtf((float)p.d);
     // |R_l| <= |union of S_l' for l' >= l| <= min(T_c, (L - l) k); the device
     // count decides which workgroups run.

@@ -32,8 +32,21 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
                               const void* q_new, const void* k_new, const void* v_new,
                               void* out, float* lse_out, int context_mode, hipStream_t st);
 
-// Tile constants of the bf16 MFMA attention kernel.
-constexpr int kAttnRows = 128;      // (target, head) rows per workgroup: 4 waves x 32
-constexpr int kAttnKeys = 64;       // keys per LDS tile
+// Tile configuration of the bf16 MFMA attention kernel (compile-time; the
+// defaults are the tuned MI355X configuration).
+#ifndef RELAXKV_ATTN_WAVES
+#define RELAXKV_ATTN_WAVES 8        // waves per workgroup
+#endif
+#ifndef RELAXKV_ATTN_TILE
+#define RELAXKV_ATTN_TILE 128       // keys per LDS tile (double-buffered)
+#endif
+#ifndef RELAXKV_ATTN_SCHED
+#define RELAXKV_ATTN_SCHED 1        // interleave K-fragment LDS reads with the QK^T MFMAs
+#endif
+#ifndef RELAXKV_ATTN_ROWBLOCKS
+#define RELAXKV_ATTN_ROWBLOCKS 1    // 32-row MFMA blocks per wave
+#endif
+// (target, head) rows per workgroup: a GQA group of G heads must fit.
+constexpr int kAttnRows = RELAXKV_ATTN_WAVES * RELAXKV_ATTN_ROWBLOCKS * 32;
 
 }  // namespace relaxkv

@@ -22,7 +22,7 @@ bool dims_ok(const relaxkv_problem* p) {
 
 // Byte sizes of the set arrays, in carving order.
 struct SetsLayout {
-    size_t anchors, h, U, cidx, R_off, R_idx, R_u, src, counts, edges, total;
+    size_t anchors, h, U, cidx, R_off, R_idx, R_u, src, rank, counts, edges, total;
 };
 
 SetsLayout sets_layout(const relaxkv_problem* p, int32_t k) {
@@ -36,9 +36,10 @@ SetsLayout sets_layout(const relaxkv_problem* p, int32_t k) {
     s.R_idx = align_up(L * T * 4);
     s.R_u = align_up(L * T * 4);
     s.src = align_up(L * T * 4);
+    s.rank = align_up(L * T * 4);
     s.counts = align_up((L + 2) * 4);
     s.edges = align_up(2 * L * 8);
-    s.total = s.anchors + s.h + s.U + s.cidx + s.R_off + s.R_idx + s.R_u + s.src + s.counts +
+    s.total = s.anchors + s.h + s.U + s.cidx + s.R_off + s.R_idx + s.R_u + s.src + s.rank + s.counts +
               s.edges;
     return s;
 }
@@ -46,7 +47,7 @@ SetsLayout sets_layout(const relaxkv_problem* p, int32_t k) {
 bool sets_match(const relaxkv_problem* p, const relaxkv_sets* s) {
     return s && s->L == p->L && s->T_c == p->T_c &&
            s->k == relaxkv_anchor_count(p->anchor_ratio, p->T_c) && s->anchors && s->h &&
-           s->U && s->cidx && s->R_off && s->R_idx && s->R_u && s->src && s->counts &&
+           s->U && s->cidx && s->R_off && s->R_idx && s->R_u && s->src && s->rank && s->counts &&
            s->edges;
 }
 
@@ -85,7 +86,7 @@ relaxkv_status relaxkv_validate(const relaxkv_problem* p) {
     if (p->dtype != RELAXKV_DTYPE_F32 && p->dtype != RELAXKV_DTYPE_BF16)
         return RELAXKV_EUNSUPPORTED;
     if (p->d != 64 && p->d != 128) return RELAXKV_EUNSUPPORTED;
-    // The bf16 attention tile packs whole GQA groups into 128 rows.
+    // The bf16 attention tile packs whole GQA groups into kAttnRows rows.
     if (p->dtype == RELAXKV_DTYPE_BF16 && p->H / p->H_kv > kAttnRows) return RELAXKV_EUNSUPPORTED;
     return RELAXKV_OK;
 }
@@ -122,6 +123,7 @@ relaxkv_status relaxkv_sets_bind(const relaxkv_problem* p, void* dev_buf, size_t
     s.R_idx = (int32_t*)b; b += l.R_idx;
     s.R_u = (int32_t*)b; b += l.R_u;
     s.src = (int32_t*)b; b += l.src;
+    s.rank = (int32_t*)b; b += l.rank;
     s.counts = (int32_t*)b; b += l.counts;
     s.edges = (int64_t*)b;
     *out = s;

@@ -18,9 +18,12 @@ namespace {
 constexpr int kSetThreads = 1024;
 constexpr int kSetPerThread = 8;
 
-__global__ void sets_reset(int32_t* __restrict__ h, int T) {
+__global__ void sets_reset(int32_t* __restrict__ h, int T, int32_t* __restrict__ rank, long n_rank) {
     for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < T; i += gridDim.x * blockDim.x)
         h[i] = -1;
+    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_rank;
+         i += (long)gridDim.x * blockDim.x)
+        rank[i] = -1;
 }
 
 __global__ void sets_mark(const int32_t* __restrict__ anchors, int L, int k, int T,
@@ -102,7 +105,7 @@ __global__ __launch_bounds__(kSetThreads) void sets_layers(
     const int32_t* __restrict__ h, const int32_t* __restrict__ U, int T,
     const int32_t* __restrict__ R_off, const int32_t* __restrict__ counts,
     int32_t* __restrict__ R_idx, int32_t* __restrict__ R_u, int32_t* __restrict__ src,
-    int64_t* __restrict__ edges, int L) {
+    int32_t* __restrict__ rank, int64_t* __restrict__ edges, int L) {
     __shared__ int scan_scratch[kSetThreads / 64];
     __shared__ long long red[2][kSetThreads / 64];
     const int l = blockIdx.x;
@@ -110,6 +113,7 @@ __global__ __launch_bounds__(kSetThreads) void sets_layers(
     const int nU = counts[0];
     const int off = R_off[l];
     int32_t* src_l = src + (size_t)l * T;
+    int32_t* rank_l = rank + (size_t)l * T;
     long long e_sum = 0, ef_sum = 0;
     int r_base = 0;
     for (int base = 0; base < nU; base += kSetThreads * kSetPerThread) {
@@ -134,6 +138,7 @@ __global__ __launch_bounds__(kSetThreads) void sets_layers(
                 R_idx[off + r] = pos[e];
                 R_u[off + r] = c;
                 src_l[c] = r;
+                rank_l[pos[e]] = r;
                 ++r;
                 e_sum += c + 1;          // |C_l(p)| = compact index of p + 1
                 ef_sum += pos[e] + 1;    // full causal prefix
@@ -166,8 +171,10 @@ __global__ __launch_bounds__(kSetThreads) void sets_layers(
 
 hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s, hipStream_t st) {
     const int T = p.T_c, L = p.L;
-    const int rb = (T + 255) / 256;
-    hipLaunchKernelGGL(sets_reset, dim3(rb < 1024 ? rb : 1024), dim3(256), 0, st, s.h, T);
+    const long n_rank = (long)L * T;
+    const long rb = (n_rank + 255) / 256;
+    hipLaunchKernelGGL(sets_reset, dim3(rb < 2048 ? (int)rb : 2048), dim3(256), 0, st, s.h, T,
+                       s.rank, n_rank);
     const long nm = (long)L * s.k;
     const long mb = (nm + 255) / 256;
     hipLaunchKernelGGL(sets_mark, dim3(mb < 2048 ? (int)mb : 2048), dim3(256), 0, st, s.anchors,
@@ -175,7 +182,7 @@ hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s, hi
     hipLaunchKernelGGL(sets_union, dim3(1), dim3(kSetThreads), 0, st, s.h, T, L, s.U, s.cidx,
                        s.R_off, s.counts);
     hipLaunchKernelGGL(sets_layers, dim3(L), dim3(kSetThreads), 0, st, s.h, s.U, T, s.R_off,
-                       s.counts, s.R_idx, s.R_u, s.src, s.edges, L);
+                       s.counts, s.R_idx, s.R_u, s.src, s.rank, s.edges, L);
     return hipGetLastError();
 }
 

@@ -45,7 +45,8 @@ class Sets(Structure):
     _fields_ = [("L", c_int32), ("T_c", c_int32), ("k", c_int32),
                 ("anchors", c_void_p), ("h", c_void_p), ("U", c_void_p), ("cidx", c_void_p),
                 ("R_off", c_void_p), ("R_idx", c_void_p), ("R_u", c_void_p),
-                ("src", c_void_p), ("counts", c_void_p), ("edges", c_void_p)]
+                ("src", c_void_p), ("rank", c_void_p), ("counts", c_void_p),
+                ("edges", c_void_p)]
 
 
 _lib = None
@@ -217,6 +218,7 @@ class SetsBuffer:
         self.R_idx = view(s.R_idx, L * T, torch.int32)
         self.R_u = view(s.R_u, L * T, torch.int32)
         self.src = view(s.src, L * T, torch.int32).view(L, T)
+        self.rank = view(s.rank, L * T, torch.int32).view(L, T)
         self.counts = view(s.counts, L + 2, torch.int32)
         self.edges = view(s.edges, 2 * L, torch.int64)
 

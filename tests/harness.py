@@ -77,7 +77,8 @@ class Case:
             R_off=R_off,
             R=[R_idx[R_off[l]:R_off[l + 1]] for l in range(L)],
             R_u=[R_u[R_off[l]:R_off[l + 1]] for l in range(L)],
-            src=[src[l, :nU] for l in range(L)])
+            src=[src[l, :nU] for l in range(L)],
+            rank=self.sets.rank.cpu().numpy())
 
     def fresh(self, layer, R_l):
         """Compact fresh rows of the targets R_l of one layer (device tensors)."""
@@ -118,6 +119,9 @@ def compare_sets(got, ref):
         assert got["R"][l].tolist() == ref.R[l].tolist(), l
         assert got["R_u"][l].tolist() == ref.R_u[l].tolist(), l
         assert got["src"][l].tolist() == ref.src[l].tolist(), l
+        rank = np.full(ref.T_c, -1)
+        rank[ref.R[l]] = np.arange(len(ref.R[l]))
+        assert got["rank"][l].tolist() == rank.tolist(), l
         assert got["edges"][l] == int(ref.edges[l]), l
         assert got["edges"][L + l] == int(ref.edges_full[l]), l
     assert got["counts"][L + 1] == 0

@@ -83,8 +83,8 @@ def _problem(rk, **kw):
     ({"anchor_ratio": -0.5}, -1), ({"anchor_ratio": float("nan")}, -1),
     ({"softmax_scale": float("nan")}, -1), ({"softmax_scale": float("inf")}, -1),
     ({"d": 96}, -3), ({"d": 256}, -3), ({"dtype": 7}, -3),
-    ({"H": 256, "H_kv": 1}, -3),                      # a GQA group wider than the bf16 tile
-    ({"H": 256, "H_kv": 1, "dtype": 0}, 0),           # fp32 kernels have no such limit
+    ({"H": 512, "H_kv": 1}, -3),                      # a GQA group wider than the bf16 tile
+    ({"H": 512, "H_kv": 1, "dtype": 0}, 0),           # fp32 kernels have no such limit
     ({"d": 64, "dtype": 0}, 0),
 ])
 def test_validate(rk, kw, status):
@@ -103,7 +103,7 @@ def test_sizes(rk):
     sb = lib.relaxkv_sets_bytes(ctypes.byref(p))
     L, T, k = 4, 2048, oracle_anchor_count(0.15, 2048)
     assert ws >= L * 2 * T * 4                      # per-KV-head partial sums
-    assert sb >= 4 * (L * k + 3 * T + (L + 1) + 3 * L * T + (L + 2)) + 8 * 2 * L
+    assert sb >= 4 * (L * k + 3 * T + (L + 1) + 4 * L * T + (L + 2)) + 8 * 2 * L
     assert sb % 256 == 0 and ws % 256 == 0
     bad = _problem(rk, d=96)
     assert lib.relaxkv_score_workspace_bytes(ctypes.byref(bad)) == 0
@@ -119,12 +119,13 @@ def test_sets_bind_carves_buffer(rk):
     assert lib.relaxkv_sets_bind(ctypes.byref(p), ctypes.c_void_p(base), nbytes,
                                  ctypes.byref(s)) == 0
     assert (s.L, s.T_c, s.k) == (4, 2048, oracle_anchor_count(0.15, 2048))
-    ptrs = [s.anchors, s.h, s.U, s.cidx, s.R_off, s.R_idx, s.R_u, s.src, s.counts, s.edges]
+    ptrs = [s.anchors, s.h, s.U, s.cidx, s.R_off, s.R_idx, s.R_u, s.src, s.rank, s.counts,
+            s.edges]
     assert ptrs[0] == base and ptrs == sorted(ptrs)
     assert all(x % 256 == 0 for x in ptrs)
     L, T, k = s.L, s.T_c, s.k
     sizes = [L * k * 4, T * 4, T * 4, T * 4, (L + 1) * 4, L * T * 4, L * T * 4, L * T * 4,
-             (L + 2) * 4, 2 * L * 8]
+             L * T * 4, (L + 2) * 4, 2 * L * 8]
     for a, b, n in zip(ptrs, ptrs[1:] + [base + nbytes], sizes):
         assert b - a >= n
     assert lib.relaxkv_sets_bind(ctypes.byref(p), ctypes.c_void_p(base), nbytes - 1,
