@@ -99,7 +99,7 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
     constexpr int KS = D / 16;             // k-steps of the QK^T contraction
     constexpr int DB = D / 32;             // 32-wide d blocks of O^T
     constexpr int KSTR = D + 8;            // K tile row stride (elements)
-    constexpr int VSTR = D + 16;           // V tile row stride (elements): rows 8 banks apart
+    constexpr int VSTR = D + RELAXKV_ATTN_VPAD;   // V tile row stride (elements)
     constexpr int P = D / 8;               // 16-byte parts per row
     constexpr int KPT = BN * P / NT;       // keys per thread in the loader
     static_assert(KPT >= 1 && BN * P == KPT * NT, "loader shape");
@@ -226,28 +226,53 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
             f32x16 s[RB][2];
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x16{};
-            // K fragments are read two k-steps ahead of the MFMAs that use them.
-            bf16x8 kf[KS][2];
+#if RELAXKV_ATTN_SETPRIO
+            __builtin_amdgcn_s_setprio(2);
+#endif
+            // K fragments are read ahead of the MFMAs that use them: with one row
+            // block all 2*KS fragments are issued first; with two row blocks (each
+            // fragment feeds two MFMAs) a ring of two k-steps keeps registers low.
+            if constexpr (RB == 1) {
+                bf16x8 kf[KS][2];
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                kf[ks][0] = *(const bf16x8*)(kst + r32 * KSTR + ks * 16 + hf * 8);
-                kf[ks][1] = *(const bf16x8*)(kst + (32 + r32) * KSTR + ks * 16 + hf * 8);
-            }
+                for (int ks = 0; ks < KS; ++ks) {
+                    kf[ks][0] = *(const bf16x8*)(kst + r32 * KSTR + ks * 16 + hf * 8);
+                    kf[ks][1] = *(const bf16x8*)(kst + (32 + r32) * KSTR + ks * 16 + hf * 8);
+                }
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
+                for (int ks = 0; ks < KS; ++ks) {
+                    s[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][0], qf[0][ks], s[0][0], 0, 0, 0);
+                    s[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][1], qf[0][ks], s[0][1], 0, 0, 0);
+                }
+#if RELAXKV_ATTN_SCHED
+                __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // 4 LDS reads
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb) {
-                    s[rb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][0], qf[rb][ks], s[rb][0], 0, 0, 0);
-                    s[rb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][1], qf[rb][ks], s[rb][1], 0, 0, 0);
+                for (int ks = 0; ks < KS; ++ks) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMAs
+                    if (ks + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                }
+#endif
+            } else {
+                bf16x8 ka[2], kb[2];
+                ka[0] = *(const bf16x8*)(kst + r32 * KSTR + hf * 8);
+                ka[1] = *(const bf16x8*)(kst + (32 + r32) * KSTR + hf * 8);
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    if (ks + 1 < KS) {
+                        kb[0] = *(const bf16x8*)(kst + r32 * KSTR + (ks + 1) * 16 + hf * 8);
+                        kb[1] = *(const bf16x8*)(kst + (32 + r32) * KSTR + (ks + 1) * 16 + hf * 8);
+                    }
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb) {
+                        s[rb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qf[rb][ks], s[rb][0], 0, 0, 0);
+                        s[rb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qf[rb][ks], s[rb][1], 0, 0, 0);
+                    }
+                    ka[0] = kb[0];
+                    ka[1] = kb[1];
                 }
             }
-#if RELAXKV_ATTN_SCHED
-            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // 4 LDS reads
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 2 * RB, 0);
-                if (ks + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-            }
+#if RELAXKV_ATTN_SETPRIO
+            __builtin_amdgcn_s_setprio(0);
 #endif
             if (c0 + 63 > cmin) {                          // staircase step: mask
 #pragma unroll
@@ -300,6 +325,9 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
                 l_run[rb] += ls;
             }
             // O^T += V^T P^T
+#if RELAXKV_ATTN_SETPRIO
+            __builtin_amdgcn_s_setprio(2);
+#endif
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -319,6 +347,9 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
                     }
                 }
             }
+#if RELAXKV_ATTN_SETPRIO
+            __builtin_amdgcn_s_setprio(0);
+#endif
         }
     }
 

@@ -43,6 +43,12 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
 #ifndef RELAXKV_ATTN_SCHED
 #define RELAXKV_ATTN_SCHED 1        // interleave K-fragment LDS reads with the QK^T MFMAs
 #endif
+#ifndef RELAXKV_ATTN_SETPRIO
+#define RELAXKV_ATTN_SETPRIO 1      // raise wave priority during MFMA phases
+#endif
+#ifndef RELAXKV_ATTN_VPAD
+#define RELAXKV_ATTN_VPAD 32        // V tile row padding (elements): conflict-free transposing reads
+#endif
 #ifndef RELAXKV_ATTN_ROWBLOCKS
 #define RELAXKV_ATTN_ROWBLOCKS 1    // 32-row MFMA blocks per wave
 #endif
