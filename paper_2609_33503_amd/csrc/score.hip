@@ -3,16 +3,18 @@
 //   p_{l,i} = (1/(H Qn)) sum_{h,t} A_l[h,t,i],   a_{l,i} = MinMax_i(p_{l,i}).
 //
 // bf16 path (bf16 MFMA, fp32 accumulation), per layer l and KV head g the
-// Qn*G query rows that share g form one row set:
-//   1. score_stats  -- key splits of 512 keys; each of 8 waves keeps 64 keys
-//      of K in registers and streams the row set's Q through LDS, computing
-//      S^T = K Q^T (one query row per lane) and each row's (max, sum of exp2)
-//      over its keys.                                    [skipped with q_lse]
+// Qn*G query rows that share g form one row set; each workgroup takes a split
+// of 1024 contiguous keys, each wave holds one 32-row block of the row set's
+// queries in registers, and 128-key tiles of K stream through double-buffered
+// LDS:
+//   1. score_pass<STATS> -- S^T = K Q^T (one query row per lane) and each
+//      row's (max, sum of exp2) over the split.          [skipped with q_lse]
 //   2. score_merge  -- per row, merge the splits into a log2-sum-exp.
-//   3. score_colsum -- the same tiles as S = Q K^T (one key per lane): every
-//      lane sums exp2(s - lse) over its rows, giving the pooled mass of its key
-//      for this KV head.  K is read once more (from the last-level cache when
-//      the layer's K fits there).
+//   3. score_pass<colsum> -- the same tiles as S = Q K^T (one key per lane):
+//      every lane sums exp2(s - lse) over its rows, the waves' partial sums are
+//      added in a fixed order, giving the pooled mass of each key for this KV
+//      head.  K is read once more (from the last-level cache when the layer's
+//      K fits there).
 //   4. score_finalize -- per layer, the fixed-order sum over KV heads, the
 //      1/(H Qn) factor and the MinMax normalisation.
 // float32 path: plain VALU kernels with the same four steps (used for fp32
@@ -28,120 +30,193 @@
 namespace relaxkv {
 namespace {
 
-constexpr int kScoreWaves = 8;
-constexpr int kScoreThreads = kScoreWaves * 64;
-constexpr int kKeysPerWave = 64;
-constexpr int kKeysPerSplit = kScoreWaves * kKeysPerWave;   // 512
-constexpr int kRowChunk = 384;                              // query rows staged in LDS at once
+constexpr int kTileKeys = 128;                 // keys per LDS tile
+constexpr int kTilesPerSplit = 8;              // tiles per workgroup
+constexpr int kKeysPerSplit = kTileKeys * kTilesPerSplit;   // 1024 keys per workgroup
+constexpr int kMaxWaves = 10;                  // row blocks per workgroup (one per wave)
 
 __host__ __device__ inline int round_up32(int x) { return (x + 31) / 32 * 32; }
 
-template <int D>
-__device__ __forceinline__ void load_k_frags(const uint16_t* __restrict__ Kg, int c0, int T,
-                                             int r32, int hf, bf16x8 (&kf)[2][D / 16]) {
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-        const int key = c0 + kb * 32 + r32;
-#pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-            if (key < T)
-                kf[kb][ks] = *(const bf16x8*)(Kg + (size_t)key * D + ks * 16 + hf * 8);
-            else
-                kf[kb][ks] = bf16x8{};
-        }
-    }
+// The copy of a value held by the lane 32 away.  v_permlane32_swap with both
+// operands x returns, in each lane, x and its partner's x in its two results;
+// xor-ing both results with x leaves the partner's bits whichever result holds
+// which.
+__device__ __forceinline__ float pair_other(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __uint_as_float(r[0] ^ r[1] ^ u);
 }
 
-// Stage rows rc0 .. rc0+nrows-1 of the row set (row rho = t*G + hh reads
-// q[l][t][g*G + hh][:]) into LDS with a padded stride; rows >= n_rows are zero.
-template <int D>
-__device__ __forceinline__ void stage_q(const uint16_t* __restrict__ q, uint16_t* Qs, int l,
-                                        int g, int rc0, int nrows, int n_rows, int Qn, int H,
-                                        int G) {
-    constexpr int QSTR = D + 8;
-    constexpr int P = D / 8;
-    for (int idx = threadIdx.x; idx < nrows * P; idx += blockDim.x) {
-        const int rr = idx / P, part = idx % P;
-        const int rho = rc0 + rr;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (rho < n_rows) {
-            const int t = rho / G, hh = rho % G;
-            v = *(const u32x4*)(q + (((size_t)l * Qn + t) * H + g * G + hh) * D + part * 8);
-        }
-        *(u32x4*)(Qs + rr * QSTR + part * 8) = v;
-    }
-}
-
-template <int D>
-__global__ __launch_bounds__(kScoreThreads) void score_stats_bf16(
+// One pass over the keys of a 1024-key split for the row set (l, g).  NW waves
+// each hold one 32-row block of the row set's queries in registers (row rho =
+// t*G + hh reads q[l][t][g*G + hh][:]); K tiles of 128 contiguous keys stream
+// through double-buffered LDS.
+//   STATS: S^T = K Q^T (one query row per lane): per-lane online (max, sum of
+//          exp2) over its keys, merged with the lane 32 away at the end ->
+//          stats[l][g][split][row] in log2 units.
+//   else:  S = Q K^T (one key per lane): per-lane sum of exp2(s - lse) over its
+//          16 rows, the two half-waves added, then a fixed-order sum over the
+//          waves in LDS -> part[l][g][key].
+template <int D, int NW, bool STATS>
+__global__ __launch_bounds__(NW * 64) void score_pass_bf16(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
-    int Hkv, int G, int n_rows, int rows_pad, int n_split, float scale_log2,
-    float2* __restrict__ stats) {
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    constexpr int KS = D / 16, QSTR = D + 8;
-    uint16_t* Qs = (uint16_t*)smem;
-    const int chunk_cap = rows_pad < kRowChunk ? rows_pad : kRowChunk;
-    float2* wst = (float2*)(smem + (size_t)chunk_cap * QSTR * 2);   // [waves][chunk_cap]
+    int Hkv, int G, int n_rows, int rows_pad, int n_split, float sl2,
+    float2* __restrict__ stats, const float* __restrict__ lse2, const float* __restrict__ q_lse,
+    float* __restrict__ part) {
+    constexpr int NT = NW * 64;
+    constexpr int KS = D / 16;
+    constexpr int KSTR = D + 8;
+    constexpr int P = D / 8;
+    constexpr int NB = kTileKeys / 32;
+    constexpr int CHUNKS = kTileKeys * P;          // 16-byte chunks per tile
+    constexpr int CPT = (CHUNKS + NT - 1) / NT;     // chunks per thread
+    constexpr int RING = 4;                         // K fragments read ahead
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kTileKeys * KSTR];
+    __shared__ float colp[2][STATS ? 1 : NW][kTileKeys];
 
     const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, r32 = lane & 31, hf = lane >> 5;
-    const int c0 = split * kKeysPerSplit + w * kKeysPerWave;
     const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
+    const int key0 = split * kKeysPerSplit;
+    const int ntile = min(kTilesPerSplit, (T - key0 + kTileKeys - 1) / kTileKeys);
 
-    bf16x8 kf[2][KS];
-    load_k_frags<D>(Kg, c0, T, r32, hf, kf);
-
-    for (int rc0 = 0; rc0 < rows_pad; rc0 += kRowChunk) {
-        const int nrows = rows_pad - rc0 < kRowChunk ? rows_pad - rc0 : kRowChunk;
-        __syncthreads();
-        stage_q<D>(q, Qs, l, g, rc0, nrows, n_rows, Qn, H, G);
-        __syncthreads();
-        for (int rb = 0; rb < nrows / 32; ++rb) {
-            f32x16 acc0 = {}, acc1 = {};
+    u32x4 st[CPT];
+    auto load_tile = [&](int tt) {
+        const int kbase = key0 + tt * kTileKeys;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 qf = *(const bf16x8*)(Qs + (rb * 32 + r32) * QSTR + ks * 16 + hf * 8);
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0][ks], qf, acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[1][ks], qf, acc1, 0, 0, 0);
-            }
-            // acc_kb[v] = S[row rb*32 + r32][key c0 + kb*32 + 8(v/4) + 4hf + v%4]
-            float x[32];
+        for (int i = 0; i < CPT; ++i) {
+            const int c = tid + i * NT;
+            const int key = kbase + c / P;
+            st[i] = (c < CHUNKS && key < T) ? *(const u32x4*)(Kg + (size_t)key * D + (c % P) * 8)
+                                            : u32x4{0u, 0u, 0u, 0u};
+        }
+    };
+    auto reduce_cols = [&](int tt, bool first_chunk) {   // phase 2: sum over waves
+        const int key = key0 + tt * kTileKeys + tid;
+        if (tid < kTileKeys && key < T) {
+            float v = 0.f;
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) v += colp[tt & 1][STATS ? 0 : ww][tid];
+            float* dst = part + ((size_t)l * Hkv + g) * T + key;
+            *dst = first_chunk ? v : *dst + v;
+        }
+    };
+
+    for (int rc0 = 0; rc0 < rows_pad; rc0 += NW * 32) {
+        // This lane's query fragments (row rho, k-half hf).
+        const int rho = rc0 + w * 32 + r32;
+        bf16x8 qf[KS];
+        if (rho < n_rows) {
+            const int t = rho / G, hh = rho % G;
+            const uint16_t* qrow = q + (((size_t)l * Qn + t) * H + g * G + hh) * D;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) qf[ks] = bf16x8{};
+        }
+        // Phase 2: log2-sum-exp of the 16 rows this lane accumulates
+        // (rows rc0 + w*32 + 8j + 4hf + i); padding rows get +inf.
+        float lr[16];
+        if constexpr (!STATS) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int key = c0 + 8 * (v >> 2) + 4 * hf + (v & 3);
-                x[v] = key < T ? acc0[v] * scale_log2 : -INFINITY;
-                x[16 + v] = key + 32 < T ? acc1[v] * scale_log2 : -INFINITY;
+                const int row = rc0 + w * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
+                float x = INFINITY;
+                if (row < n_rows) {
+                    x = q_lse ? q_lse[((size_t)l * Qn + row / G) * H + g * G + row % G] * kLog2e
+                              : lse2[((size_t)l * Hkv + g) * rows_pad + row];
+                }
+                lr[v] = x;
             }
-            float m = -INFINITY;
-#pragma unroll
-            for (int v = 0; v < 32; ++v) m = fmaxf(m, x[v]);
-            float z = 0.f;
-            if (m != -INFINITY) {
-#pragma unroll
-                for (int v = 0; v < 32; ++v) z += fast_exp2(x[v] - m);
-            }
-            const float m2 = swap_half(m), z2 = swap_half(z);
-            const float M = fmaxf(m, m2);
-            float Z = 0.f;
-            if (M != -INFINITY) {
-                Z = (m == -INFINITY ? 0.f : z * fast_exp2(m - M)) +
-                    (m2 == -INFINITY ? 0.f : z2 * fast_exp2(m2 - M));
-            }
-            if (hf == 0) wst[w * chunk_cap + rb * 32 + r32] = make_float2(M, Z);
         }
-        __syncthreads();
-        for (int rr = tid; rr < nrows; rr += kScoreThreads) {
-            float M = -INFINITY;
-            for (int ww = 0; ww < kScoreWaves; ++ww) M = fmaxf(M, wst[ww * chunk_cap + rr].x);
-            float Z = 0.f;
-            if (M != -INFINITY) {
-                for (int ww = 0; ww < kScoreWaves; ++ww) {
-                    const float2 s = wst[ww * chunk_cap + rr];
-                    if (s.x != -INFINITY) Z += s.y * fast_exp2(s.x - M);
+        float m_run = -INFINITY, z_run = 0.f;
+
+        __syncthreads();                                // LDS free from the previous row chunk
+        load_tile(0);
+        for (int tt = 0; tt < ntile; ++tt) {
+            uint16_t* kb = Ks[tt & 1];
+#pragma unroll
+            for (int i = 0; i < CPT; ++i) {
+                const int c = tid + i * NT;
+                if (c < CHUNKS) *(u32x4*)(kb + (c / P) * KSTR + (c % P) * 8) = st[i];
+            }
+            __syncthreads();
+            if (!STATS && tt > 0) reduce_cols(tt - 1, rc0 == 0);
+            if (tt + 1 < ntile) load_tile(tt + 1);
+
+            const int kbase = key0 + tt * kTileKeys;
+            // Two 32-key blocks at a time (two independent MFMA chains), K
+            // fragments read RING MFMAs ahead.
+#pragma unroll
+            for (int bp = 0; bp < NB / 2; ++bp) {
+                f32x16 acc[2] = {f32x16{}, f32x16{}};
+                const uint16_t* kp = kb + (64 * bp + r32) * KSTR + hf * 8;
+                bf16x8 kf[RING];
+#pragma unroll
+                for (int i = 0; i < RING; ++i) kf[i] = *(const bf16x8*)(kp + (i & 1) * 32 * KSTR + (i >> 1) * 16);
+#pragma unroll
+                for (int sx = 0; sx < 2 * KS; ++sx) {
+                    const int ks = sx >> 1, i = sx & 1;
+                    const bf16x8 cur = kf[sx % RING];
+                    if (sx + RING < 2 * KS) {
+                        const int s2 = sx + RING;
+                        kf[sx % RING] = *(const bf16x8*)(kp + (s2 & 1) * 32 * KSTR + (s2 >> 1) * 16);
+                    }
+                    if constexpr (STATS)
+                        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[ks], acc[i], 0, 0, 0);
+                    else
+                        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], cur, acc[i], 0, 0, 0);
+                }
+                const int kb0 = kbase + 64 * bp;
+                if constexpr (STATS) {
+                    // acc[i][v] = S[row r32][key kb0 + 32i + 8(v/4) + 4hf + v%4]
+                    if (kb0 + 64 > T) {
+#pragma unroll
+                        for (int i = 0; i < 2; ++i)
+#pragma unroll
+                            for (int v = 0; v < 16; ++v)
+                                if (kb0 + 32 * i + 8 * (v >> 2) + 4 * hf + (v & 3) >= T)
+                                    acc[i][v] = -INFINITY;
+                    }
+                    float mt = fmaxf(acc[0][0], acc[1][0]);
+#pragma unroll
+                    for (int v = 1; v < 16; ++v) mt = fmaxf(mt, fmaxf(acc[0][v], acc[1][v]));
+                    const float m_new = fmaxf(m_run, mt * sl2);
+                    const float mref = m_new == -INFINITY ? 0.f : m_new;
+                    float z = z_run * fast_exp2(m_run - mref);
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) z += fast_exp2(fmaf(acc[i][v], sl2, -mref));
+                    z_run = z;
+                    m_run = m_new;
+                } else {
+                    // acc[i][v] = S[row rc0 + w*32 + 8(v/4) + 4hf + v%4][key kb0 + 32i + r32]
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) {
+                        float cs = 0.f;
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) cs += fast_exp2(fmaf(acc[i][v], sl2, -lr[v]));
+                        const float other = pair_other(cs);
+                        if (hf == 0) colp[tt & 1][STATS ? 0 : w][64 * bp + 32 * i + r32] = cs + other;
+                    }
                 }
             }
-            stats[(((size_t)l * Hkv + g) * n_split + split) * rows_pad + rc0 + rr] =
-                make_float2(M, Z);
+        }
+        if constexpr (STATS) {
+            // merge with the lane 32 away (same row, the other half of the keys)
+            const float m2 = pair_other(m_run), z2 = pair_other(z_run);
+            const float M = fmaxf(m_run, m2);
+            float Z = 0.f;
+            if (M != -INFINITY)
+                Z = (m_run == -INFINITY ? 0.f : z_run * fast_exp2(m_run - M)) +
+                    (m2 == -INFINITY ? 0.f : z2 * fast_exp2(m2 - M));
+            if (hf == 0 && rho < rows_pad)
+                stats[(((size_t)l * Hkv + g) * n_split + split) * rows_pad + rho] = make_float2(M, Z);
+        } else {
+            __syncthreads();
+            reduce_cols(ntile - 1, rc0 == 0);
         }
     }
 }
@@ -165,68 +240,6 @@ __global__ void score_merge(const float2* __restrict__ stats, int n_groups, int 
         if (v.x != -INFINITY) Z += v.y * fast_exp2(v.x - M);
     }
     lse2[i] = M + __log2f(Z);
-}
-
-template <int D>
-__global__ __launch_bounds__(kScoreThreads) void score_colsum_bf16(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
-    int Hkv, int G, int n_rows, int rows_pad, float scale_log2, const float* __restrict__ lse2,
-    const float* __restrict__ q_lse, float* __restrict__ part) {
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    constexpr int KS = D / 16, QSTR = D + 8;
-    uint16_t* Qs = (uint16_t*)smem;
-    const int chunk_cap = rows_pad < kRowChunk ? rows_pad : kRowChunk;
-    float* ls = (float*)(smem + (size_t)chunk_cap * QSTR * 2);     // [chunk_cap]
-
-    const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, r32 = lane & 31, hf = lane >> 5;
-    const int c0 = split * kKeysPerSplit + w * kKeysPerWave;
-    const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
-
-    bf16x8 kf[2][KS];
-    load_k_frags<D>(Kg, c0, T, r32, hf, kf);
-    float cs0 = 0.f, cs1 = 0.f;
-
-    for (int rc0 = 0; rc0 < rows_pad; rc0 += kRowChunk) {
-        const int nrows = rows_pad - rc0 < kRowChunk ? rows_pad - rc0 : kRowChunk;
-        __syncthreads();
-        stage_q<D>(q, Qs, l, g, rc0, nrows, n_rows, Qn, H, G);
-        for (int rr = tid; rr < nrows; rr += kScoreThreads) {
-            const int rho = rc0 + rr;
-            float v;
-            if (rho >= n_rows) v = INFINITY;
-            else if (q_lse) v = q_lse[((size_t)l * Qn + rho / G) * H + g * G + rho % G] * kLog2e;
-            else v = lse2[((size_t)l * Hkv + g) * rows_pad + rho];
-            ls[rr] = v;
-        }
-        __syncthreads();
-        for (int rb = 0; rb < nrows / 32; ++rb) {
-            f32x16 acc0 = {}, acc1 = {};
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 qf = *(const bf16x8*)(Qs + (rb * 32 + r32) * QSTR + ks * 16 + hf * 8);
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf, kf[0][ks], acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf, kf[1][ks], acc1, 0, 0, 0);
-            }
-            // acc_kb[v] = S[row rb*32 + 8(v/4) + 4hf + v%4][key c0 + kb*32 + r32]
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const f32x4 lr = *(const f32x4*)(ls + rb * 32 + 8 * j + 4 * hf);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    cs0 += fast_exp2(acc0[4 * j + i] * scale_log2 - lr[i]);
-                    cs1 += fast_exp2(acc1[4 * j + i] * scale_log2 - lr[i]);
-                }
-            }
-        }
-    }
-    cs0 += swap_half(cs0);
-    cs1 += swap_half(cs1);
-    if (hf == 0) {
-        float* out = part + ((size_t)l * Hkv + g) * T;
-        if (c0 + r32 < T) out[c0 + r32] = cs0;
-        if (c0 + 32 + r32 < T) out[c0 + 32 + r32] = cs1;
-    }
 }
 
 // ---------------------------------------------------------------- float32 path
@@ -351,38 +364,42 @@ __global__ __launch_bounds__(1024) void score_finalize(const float* __restrict__
     for (int i = tid; i < T; i += 1024) a[i] = flat ? 0.f : (a[i] - lo) / span;
 }
 
-template <int D>
-hipError_t launch_score_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws,
-                             float* scores, hipStream_t st, float scale) {
+template <int D, int NW>
+void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws,
+                        hipStream_t st, float sl2) {
     const int G = p.H / p.H_kv;
     const int n_rows = p.n_query * G;
-    const int chunk_cap = w.rows_pad < kRowChunk ? w.rows_pad : kRowChunk;
-    const size_t qbytes = (size_t)chunk_cap * (D + 8) * 2;
-    const float sl2 = scale * kLog2e;
     const uint16_t* q = (const uint16_t*)p.q;
     const uint16_t* kc = (const uint16_t*)p.k_cache;
     float* part = (float*)(ws + w.part_off);
     float* lse2 = (float*)(ws + w.lse_off);
+    float2* stats = (float2*)(ws + w.stats_off);
     const dim3 grid(w.n_split, p.H_kv, p.L);
     if (!p.q_lse) {
-        const size_t lds = qbytes + (size_t)kScoreWaves * chunk_cap * sizeof(float2);
-        hipFuncSetAttribute((const void*)score_stats_bf16<D>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(score_stats_bf16<D>, grid, dim3(kScoreThreads), lds, st, q, kc, p.T_c,
-                           p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2,
-                           (float2*)(ws + w.stats_off));
+        hipLaunchKernelGGL((score_pass_bf16<D, NW, true>), grid, dim3(NW * 64), 0, st, q, kc,
+                           p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2,
+                           stats, (const float*)nullptr, (const float*)nullptr, part);
         const long n = (long)p.L * p.H_kv * w.rows_pad;
         hipLaunchKernelGGL(score_merge, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                           (const float2*)(ws + w.stats_off), p.L * p.H_kv, w.n_split,
-                           w.rows_pad, n_rows, lse2);
+                           (const float2*)stats, p.L * p.H_kv, w.n_split, w.rows_pad, n_rows, lse2);
     }
-    const size_t lds = qbytes + (size_t)chunk_cap * sizeof(float);
-    hipFuncSetAttribute((const void*)score_colsum_bf16<D>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(score_colsum_bf16<D>, grid, dim3(kScoreThreads), lds, st, q, kc, p.T_c,
-                       p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, sl2, lse2, p.q_lse, part);
-    hipLaunchKernelGGL(score_finalize, dim3(p.L), dim3(1024), 0, st, part, w.n_part, p.T_c,
-                       1.0f / ((float)p.H * (float)p.n_query), scores);
+    hipLaunchKernelGGL((score_pass_bf16<D, NW, false>), grid, dim3(NW * 64), 0, st, q, kc, p.T_c,
+                       p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2, stats,
+                       (const float*)lse2, p.q_lse, part);
+}
+
+template <int D>
+hipError_t launch_score_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws,
+                             float* scores, hipStream_t st, float scale) {
+    const float sl2 = scale * kLog2e;
+    // One wave per 32-row block of the row set, up to kMaxWaves; larger row sets
+    // loop over row chunks of 8 blocks.
+    const int nrb = w.rows_pad / 32;
+    if (nrb <= 4) launch_passes_bf16<D, 4>(p, w, ws, st, sl2);
+    else if (nrb <= 8 || nrb > kMaxWaves) launch_passes_bf16<D, 8>(p, w, ws, st, sl2);
+    else launch_passes_bf16<D, kMaxWaves>(p, w, ws, st, sl2);
+    hipLaunchKernelGGL(score_finalize, dim3(p.L), dim3(1024), 0, st, (const float*)(ws + w.part_off),
+                       w.n_part, p.T_c, 1.0f / ((float)p.H * (float)p.n_query), scores);
     return hipGetLastError();
 }
 
