@@ -206,6 +206,24 @@ relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets*
                                    int32_t context_mode, void* stream);
 
 /*
+ * Cache update of layer `layer` (Sec. 3.4 cache-update semantics; Algorithm 1,
+ * cache-update step; App. A.2): the fresh K/V rows of the active targets R_l
+ * overwrite the layer's cache entries at their positions; every other entry
+ * keeps its value.
+ *   k_new, v_new      device [|R_l|][H_kv][d] in dtype, R_l order (the rows given
+ *                     to relaxkv_sparse_attn).
+ *   k_cache, v_cache  device [L][H_kv][T_c][d] in dtype: the cache to update in
+ *                     place.  It may be p->k_cache / p->v_cache themselves, or an
+ *                     output cache the caller initialised from them.
+ * Reads s->R_off, s->R_idx and s->counts on the device.  Rows written (positions
+ * in R_l) are never read by relaxkv_sparse_attn of the same layer, which reads
+ * cached rows only outside R_l, so the two calls need no mutual ordering.
+ */
+relaxkv_status relaxkv_update_cache(const relaxkv_problem* p, const relaxkv_sets* s,
+                                    int32_t layer, const void* k_new, const void* v_new,
+                                    void* k_cache, void* v_cache, void* stream);
+
+/*
  * Synchronising.  Copies s->counts ([L+2] int32) to host_counts and, when
  * host_edges is not NULL, s->edges ([2L] int64) to host_edges, after all work
  * queued on `stream`.  Returns RELAXKV_EINVAL when the device error word is

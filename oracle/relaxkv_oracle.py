@@ -23,6 +23,8 @@ with Sparse Context Attention for Efficient KV Cache Reuse"):
                       (mixed fresh/cached K~, V~ rule); the Full-Prefix Control
                       of App. A.3 (Table "Controlled configurations") with
                       ``mode="full"``.
+* ``update_cache`` -- Sec. 3.4 cache-update semantics, Algorithm 1 update step:
+                      fresh rows of R_l overwrite their cache positions.
 
 Readings where the paper is silent (each also listed in the design notes):
 
@@ -275,3 +277,22 @@ def attention_flops(H, d, edges):
     per edge and query head one d-long dot product (2d) and one d-long
     weighted sum (2d)."""
     return 4.0 * H * d * float(np.sum(edges))
+
+
+# ----------------------------------------------------------------------------
+# Cache update: Sec. 3.4 cache-update semantics; Algorithm 1, update step.
+# ----------------------------------------------------------------------------
+
+def update_cache(layer, sets, k_new, v_new, k_cache_l, v_cache_l):
+    """The layer's cache after repair: the fresh rows of the active targets R_l
+    overwrite their positions; every other entry keeps its value.
+
+    k_new/v_new [|R_l|][H_kv][d] in R_l order; k_cache_l/v_cache_l [H_kv][T_c][d].
+    Returns new (k, v) arrays; the inputs are not modified."""
+    R_l = sets.R[layer]
+    k = np.array(k_cache_l, copy=True)
+    v = np.array(v_cache_l, copy=True)
+    for t, p in enumerate(R_l):
+        k[:, p, :] = k_new[t]
+        v[:, p, :] = v_new[t]
+    return k, v

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "attn_config.h"
 #include "relaxkv.h"
 
 namespace relaxkv {
@@ -28,31 +29,12 @@ hipError_t launch_select(const relaxkv_problem& p, const float* scores,
                          const relaxkv_sets& s, hipStream_t st);
 hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s,
                              hipStream_t st);
+hipError_t launch_update_cache(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
+                               const void* k_new, const void* v_new, void* k_cache,
+                               void* v_cache, hipStream_t st);
 hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
                               const void* q_new, const void* k_new, const void* v_new,
                               void* out, float* lse_out, int context_mode, hipStream_t st);
 
-// Tile configuration of the bf16 MFMA attention kernel (compile-time; the
-// defaults are the tuned MI355X configuration).
-#ifndef RELAXKV_ATTN_WAVES
-#define RELAXKV_ATTN_WAVES 8        // waves per workgroup
-#endif
-#ifndef RELAXKV_ATTN_TILE
-#define RELAXKV_ATTN_TILE 128       // keys per LDS tile (double-buffered)
-#endif
-#ifndef RELAXKV_ATTN_SCHED
-#define RELAXKV_ATTN_SCHED 1        // interleave K-fragment LDS reads with the QK^T MFMAs
-#endif
-#ifndef RELAXKV_ATTN_SETPRIO
-#define RELAXKV_ATTN_SETPRIO 1      // raise wave priority during MFMA phases
-#endif
-#ifndef RELAXKV_ATTN_VPAD
-#define RELAXKV_ATTN_VPAD 32        // V tile row padding (elements): conflict-free transposing reads
-#endif
-#ifndef RELAXKV_ATTN_ROWBLOCKS
-#define RELAXKV_ATTN_ROWBLOCKS 1    // 32-row MFMA blocks per wave
-#endif
-// (target, head) rows per workgroup: a GQA group of G heads must fit.
-constexpr int kAttnRows = RELAXKV_ATTN_WAVES * RELAXKV_ATTN_ROWBLOCKS * 32;
 
 }  // namespace relaxkv

@@ -171,6 +171,18 @@ relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets*
                                        context_mode, (hipStream_t)stream));
 }
 
+relaxkv_status relaxkv_update_cache(const relaxkv_problem* p, const relaxkv_sets* s,
+                                    int32_t layer, const void* k_new, const void* v_new,
+                                    void* k_cache, void* v_cache, void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!sets_match(p, s)) return RELAXKV_EINVAL;
+    if (layer < 0 || layer >= p->L) return RELAXKV_EINVAL;
+    if (!k_new || !v_new || !k_cache || !v_cache) return RELAXKV_EINVAL;
+    return from_hip(launch_update_cache(*p, *s, layer, k_new, v_new, k_cache, v_cache,
+                                        (hipStream_t)stream));
+}
+
 relaxkv_status relaxkv_counts_to_host(const relaxkv_sets* s, int32_t* host_counts,
                                       int64_t* host_edges, void* stream) {
     if (!s || !s->counts || !s->edges || !host_counts || s->L < 1) return RELAXKV_EINVAL;

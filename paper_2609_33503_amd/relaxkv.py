@@ -24,7 +24,7 @@ CONTEXT_UNION, CONTEXT_FULL = 0, 1
 EXPORTS = ("relaxkv_status_string", "relaxkv_anchor_count", "relaxkv_validate",
            "relaxkv_score_workspace_bytes", "relaxkv_sets_bytes", "relaxkv_sets_bind",
            "relaxkv_score", "relaxkv_select", "relaxkv_build_sets", "relaxkv_sparse_attn",
-           "relaxkv_counts_to_host")
+           "relaxkv_update_cache", "relaxkv_counts_to_host")
 
 
 class RelaxKVError(RuntimeError):
@@ -83,6 +83,9 @@ def load(path=None):
     lib.relaxkv_sparse_attn.argtypes = [POINTER(Problem), POINTER(Sets), c_int32, c_void_p,
                                         c_void_p, c_void_p, c_void_p, c_void_p, c_int32,
                                         c_void_p]
+    lib.relaxkv_update_cache.restype = c_int32
+    lib.relaxkv_update_cache.argtypes = [POINTER(Problem), POINTER(Sets), c_int32, c_void_p,
+                                         c_void_p, c_void_p, c_void_p, c_void_p]
     lib.relaxkv_counts_to_host.restype = c_int32
     lib.relaxkv_counts_to_host.argtypes = [POINTER(Sets), POINTER(c_int32), POINTER(c_int64),
                                            c_void_p]
@@ -195,6 +198,20 @@ class Request:
                                           _ptr(q_new), _ptr(k_new), _ptr(v_new), _ptr(out),
                                           _ptr(lse_out), int(context_mode), _stream(stream)),
                "relaxkv_sparse_attn")
+
+
+    def update_cache(self, sets, layer, k_new, v_new, k_cache, v_cache, stream=None):
+        """Fresh rows of R_l into the cache (k_cache/v_cache: [L][H_kv][T_c][d])."""
+        for t in (k_new, v_new, k_cache, v_cache):
+            if not t.is_contiguous() or t.dtype != self.dtype:
+                raise ValueError("rows and caches must be contiguous, in the problem dtype")
+        if tuple(k_cache.shape) != tuple(self.tensors[1].shape) or \
+                tuple(v_cache.shape) != tuple(self.tensors[2].shape):
+            raise ValueError("caches must have the problem's cache shape")
+        _check(load().relaxkv_update_cache(ctypes.byref(self.p), ctypes.byref(sets.s), int(layer),
+                                           _ptr(k_new), _ptr(v_new), _ptr(k_cache),
+                                           _ptr(v_cache), _stream(stream)),
+               "relaxkv_update_cache")
 
 
 class SetsBuffer:

@@ -207,3 +207,68 @@ def test_full_size_attention_sampled(big_case, mode):
         K = np.where((rank[ctx] >= 0)[:, None], kn[np.maximum(rank[ctx], 0), g], kc[g, ctx])
         s = K @ qn[0] / math.sqrt(BIG.d)
         assert np.exp(s - float(lse[t, 0])).sum() == pytest.approx(1.0, abs=2e-3)
+
+
+# ---------------------------------------------------------------- every workload at full size
+
+@pytest.mark.parametrize("name,ratio", [("llama8b-8k", None), ("qwen14b-16k", 0.05),
+                                        ("qwen14b-16k", 0.15), ("qwen14b-16k", 0.30)])
+def test_full_size_workloads(gpu_lib, name, ratio):
+    """Full-size workloads on sampled layers: scores within tolerance; selection
+    and sets bit-exact on the oracle's fp32 scores of those layers (the other
+    layers take seeded scores); attention on sampled targets of each sampled
+    layer, in the launch configuration the benchmark uses."""
+    w = W[name]
+    case = Case(w, ratio=ratio)
+    L, T = case.L, case.T
+    layers = [0, L // 2, L - 1]
+    a_gpu = case.gpu_scores().cpu().numpy()
+    a_ref, _, _ = case.oracle_scores(layers)
+    assert_close(a_gpu[layers], a_ref, w, f"scores {name}")
+    a = synthetic_scores(L, T, seed=21)
+    a[layers] = a_ref.astype(np.float32)
+    anchors = case.gpu_select(torch.from_numpy(a).cuda())
+    anchors_ref = oracle.select(a.astype(np.float64), case.k)
+    assert np.array_equal(anchors, anchors_ref)
+    sets_ref = oracle.build_sets(anchors_ref, T)
+    compare_sets(case.gpu_sets(), sets_ref)
+    rng = np.random.default_rng(4)
+    for l in layers:
+        R_l = sets_ref.R[l]
+        n = len(R_l)
+        fresh = case.fresh(l, R_l)
+        out, lse = case.gpu_attn(l, fresh, n)
+        ts = sorted(set([0, n // 2, n - 1] + rng.integers(0, n, size=5).tolist()))
+        O_ref, lse_ref = case.oracle_attn(l, sets_ref, fresh, targets=ts)
+        assert_close(out[ts].float().cpu().numpy(), O_ref, w, f"O {name} layer {l}", rel_gate=1e-2)
+        assert_close(lse[ts].cpu().numpy(), lse_ref, w, f"lse {name} layer {l}")
+
+
+@pytest.mark.parametrize("name", ["qwen-planted", "tiny", "d64-bf16"])
+def test_update_cache_bit_exact(gpu_lib, name):
+    """The repaired cache after every layer's update equals the oracle's
+    (pure data movement: bit-exact), in place and into a separate output cache."""
+    w = SMALL[name]
+    case = Case(w)
+    a = synthetic_scores(case.L, case.T, seed=8)
+    anchors_ref = oracle.select(a.astype(np.float64), case.k)
+    sets_ref = oracle.build_sets(anchors_ref, case.T)
+    case.req.select(torch.from_numpy(a).cuda(), case.sets)
+    compare_sets(case.gpu_sets(), sets_ref)
+    k_out, v_out = case.kc.clone(), case.vc.clone()
+    for l in range(case.L):
+        R_l = sets_ref.R[l]
+        _, kn, vn = case.fresh(l, R_l)
+        case.req.update_cache(case.sets, l, kn, vn, k_out, v_out)
+        torch.cuda.synchronize()
+        kr, vr = oracle.update_cache(l, sets_ref, synth.to_f64(kn), synth.to_f64(vn),
+                                     synth.to_f64(case.kc[l]), synth.to_f64(case.vc[l]))
+        assert np.array_equal(synth.to_f64(k_out[l]), kr)
+        assert np.array_equal(synth.to_f64(v_out[l]), vr)
+    # untouched layers stay as they were when only one layer is updated in place
+    R0 = sets_ref.R[0]
+    _, kn, vn = case.fresh(0, R0)
+    k_before = case.kc.clone()
+    case.req.update_cache(case.sets, 0, kn, vn, case.kc, case.vc)
+    torch.cuda.synchronize()
+    assert torch.equal(case.kc[1:], k_before[1:])

@@ -176,6 +176,14 @@ def test_compute_calls_reject_before_launch(rk):
                                    None, 0, None) == rk.EINVAL
     assert lib.relaxkv_sparse_attn(ctypes.byref(_problem(rk, d=96)), ctypes.byref(s), 0, *args,
                                    0, None) == rk.EUNSUPPORTED
+    # update_cache
+    for layer in (-1, 4):
+        assert lib.relaxkv_update_cache(ctypes.byref(p), ctypes.byref(s), layer, fake, fake, fake,
+                                        fake, None) == rk.EINVAL
+    assert lib.relaxkv_update_cache(ctypes.byref(p), ctypes.byref(s), 0, fake, fake, None, fake,
+                                    None) == rk.EINVAL
+    assert lib.relaxkv_update_cache(ctypes.byref(other), ctypes.byref(s), 0, fake, fake, fake,
+                                    fake, None) == rk.EINVAL
     # counts_to_host
     c = (ctypes.c_int32 * 6)()
     assert lib.relaxkv_counts_to_host(None, c, None, None) == rk.EINVAL

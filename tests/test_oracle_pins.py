@@ -372,3 +372,61 @@ def test_attention_union_equals_full_prefix_when_union_covers_all():
         Of, lf = sparse_attn(l, s, qn, kn, vn, kc, vc, mode="full")
         np.testing.assert_allclose(Ou, Of, atol=1e-14)
         np.testing.assert_allclose(lu, lf, atol=1e-14)
+
+
+def test_chunk_size_does_not_change_inputs():
+    # Chunking only affects how a real cache is built; the 2048-token chunking of
+    # the matched-target control has identical inputs to the 512-token one.
+    from paper_2609_33503_amd import synth
+    a = synth.shrink(synth.WORKLOADS["qwen14b-32k-control"], T_c=700, L=2, Qn=4)
+    b = synth.shrink(synth.WORKLOADS["qwen14b-32k-control-c2048"], T_c=700, L=2, Qn=4)
+    import dataclasses
+    assert a.wid == b.wid and a.chunk != b.chunk
+    for l in range(2):
+        for x, y in zip(synth.make_cache_layer(a, l), synth.make_cache_layer(b, l)):
+            assert torch.equal(x, y)
+    assert dataclasses.replace(b, chunk=a.chunk, name=a.name) == a
+
+
+# ----------------------------------------------------------------------------
+# cache update
+# ----------------------------------------------------------------------------
+
+def test_update_cache_hand_example():
+    from oracle import update_cache
+    ex = _hand()
+    T = ex["T_c"]
+    s = build_sets(np.array(ex["anchors"]), T)
+    kc = np.arange(T, dtype=np.float64).reshape(1, T, 1)
+    vc = -kc
+    for l, R_l in enumerate(ex["R"]):
+        kn = (np.array(R_l, dtype=np.float64) + 100.0).reshape(-1, 1, 1)
+        k2, v2 = update_cache(l, s, kn, -kn, kc, vc)
+        # exactly the positions of R_l change, to their fresh rows
+        expect = [p + 100.0 if p in R_l else float(p) for p in range(T)]
+        assert k2[0, :, 0].tolist() == expect
+        assert v2[0, :, 0].tolist() == [-x for x in expect]
+        assert kc[0, :, 0].tolist() == list(range(T))          # input untouched
+
+
+def test_update_cache_then_full_prefix_attention_reads_fresh_rows():
+    # After the update, the layer's cache holds the fresh rows at R_l, so the
+    # Full-Prefix Control over the updated cache with every row "cached" gives
+    # the same output as the mixed rule over the naive cache.
+    from oracle import update_cache
+    rng = np.random.default_rng(12)
+    L, T, H, H_kv, d = 2, 30, 4, 2, 8
+    S = _random_anchors(rng, L, T, 5)
+    s = build_sets(S, T)
+    l = 0
+    n = len(s.R[l])
+    qn, kn, vn = (rng.standard_normal((n, hh, d)) for hh in (H, H_kv, H_kv))
+    kc = rng.standard_normal((H_kv, T, d))
+    vc = rng.standard_normal((H_kv, T, d))
+    O1, _ = sparse_attn(l, s, qn, kn, vn, kc, vc, mode="full")
+    k2, v2 = update_cache(l, s, kn, vn, kc, vc)
+    O2, _ = sparse_attn(l, s, qn, kn, vn, k2, v2, mode="full")
+    np.testing.assert_allclose(O1, O2, atol=1e-14)
+    # positions outside R_l keep their naive values
+    outside = np.setdiff1d(np.arange(T), s.R[l])
+    assert np.array_equal(k2[:, outside], kc[:, outside])
