@@ -78,4 +78,44 @@ __device__ __forceinline__ float wave_max(float x) {
 // Exchange a 32-bit value with the lane 32 positions away (lane ^ 32).
 __device__ __forceinline__ float swap_half(float x) { return __shfl_xor(x, 32, 64); }
 
+// ------------------------------------------------ swizzled LDS tiles (bf16)
+//
+// Tiles of rows of D bf16 values (D = 64 or 128) filled by 16-byte direct
+// global->LDS loads (global_load_lds_dwordx4): one wave-wide load writes 64 x 16
+// bytes of consecutive LDS, so tiles are unpadded and each lane picks the
+// global chunk that belongs at its slot.  Logical 16-byte chunk c of tile row r
+// is stored at chunk c ^ tile_swz<D>(r), which makes
+// - MFMA fragment reads (16 consecutive rows, one chunk per row) and
+// - transposing reads (4 consecutive rows x 4 chunks per 32 lanes)
+// hit distinct bank groups of the 256-byte LDS bank line.
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int D>
+__device__ __forceinline__ int tile_swz(int r) {
+    static_assert(D == 64 || D == 128, "tile row width");
+    if constexpr (D == 128) {
+        return ((r & 3) << 2) | ((r >> 2) & 3);              // 16 chunks per row
+    } else {
+        const int m = (r >> 1) & 7;                          // 8 chunks, 2 rows per bank line
+        return ((m & 1) << 2) | (m >> 1);
+    }
+}
+
+// 16-byte load of global memory into LDS: lane l's chunk lands at lds + 16 l.
+// lds must be wave-uniform.
+__device__ __forceinline__ void load_lds16(const void* src, void* lds) {
+    __builtin_amdgcn_global_load_lds(src, (lds_void*)lds, 16, 0, 0);
+}
+
+// Wait until at most N vector-memory loads of this wave are outstanding and
+// all its LDS accesses are done, then join the workgroup barrier.  Unlike
+// __syncthreads() this does not drain every outstanding load, so direct LDS
+// loads of later pipeline stages stay in flight.  Loads complete in order, so
+// "at most N outstanding" means every load issued before the last N is done.
+template <int N>
+__device__ __forceinline__ void wait_loads_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
 }  // namespace relaxkv

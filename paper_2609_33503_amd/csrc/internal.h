@@ -14,7 +14,9 @@ struct ScoreWorkspace {
     size_t part_off;    // float [L][n_part][T_c]   per-KV-head pooled partial sums
     size_t stats_off;   // float2 [L][H_kv][n_split][rows_pad] (max, sum) per key split, log2 units
     size_t lse_off;     // float [L][H_kv][rows_pad] row log2-sum-exp
+    size_t mm_off;      // float2 [L][n_blk] (min, max) of p per finaliser block
     size_t total;
+    int n_blk;          // finaliser blocks per layer
     int n_part;         // partial slices summed by the finaliser
     int n_split;        // key splits of the row-statistics pass
     int rows_pad;       // n_query * G rounded up to a multiple of 32

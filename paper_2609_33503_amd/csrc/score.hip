@@ -4,9 +4,9 @@
 //
 // bf16 path (bf16 MFMA, fp32 accumulation), per layer l and KV head g the
 // Qn*G query rows that share g form one row set; each workgroup takes a split
-// of 1024 contiguous keys, each wave holds one 32-row block of the row set's
-// queries in registers, and 128-key tiles of K stream through double-buffered
-// LDS:
+// of 2048 contiguous keys, each wave holds one 32-row block of the row set's
+// queries in registers, and 16 KB tiles of K stream through a 4-deep ring of
+// LDS buffers filled by direct global->LDS loads (two workgroups per CU):
 //   1. score_pass<STATS> -- S^T = K Q^T (one query row per lane) and each
 //      row's (max, sum of exp2) over the split.          [skipped with q_lse]
 //   2. score_merge  -- per row, merge the splits into a log2-sum-exp.
@@ -15,8 +15,8 @@
 //      added in a fixed order, giving the pooled mass of each key for this KV
 //      head.  K is read once more (from the last-level cache when the layer's
 //      K fits there).
-//   4. score_finalize -- per layer, the fixed-order sum over KV heads, the
-//      1/(H Qn) factor and the MinMax normalisation.
+//   4. score_pool / score_minmax -- the fixed-order sum over KV heads and the
+//      1/(H Qn) factor with per-block extrema, then the MinMax normalisation.
 // float32 path: plain VALU kernels with the same four steps (used for fp32
 // inputs, where bf16 MFMA would not meet fp32 accuracy).
 // Every reduction has a fixed order and no float atomics: results are
@@ -30,10 +30,20 @@
 namespace relaxkv {
 namespace {
 
-constexpr int kTileKeys = 128;                 // keys per LDS tile
-constexpr int kTilesPerSplit = 8;              // tiles per workgroup
-constexpr int kKeysPerSplit = kTileKeys * kTilesPerSplit;   // 1024 keys per workgroup
-constexpr int kMaxWaves = 10;                  // row blocks per workgroup (one per wave)
+constexpr int kTileBytes = 16384;             // bytes of K per LDS tile (64 keys at d = 128)
+constexpr int kKeysPerSplit = 2048;           // keys per workgroup
+constexpr int kMaxWaves = 10;                 // row blocks per workgroup (one per wave)
+constexpr int kStages = 4;                    // LDS ring of K tiles
+constexpr int kRing = 4;                      // K fragments read ahead of their MFMA
+
+template <int D>
+constexpr int tile_keys() { return kTileBytes / (2 * D); }
+
+// Two workgroups share a CU (LDS ~70 KB each), so the waves of one overlap the
+// barrier waits and vector phases of the other, and 2 x 10 waves spread evenly
+// over the 4 SIMDs.
+template <int NW>
+constexpr int score_waves_per_simd() { return (2 * NW + 3) / 4; }
 
 __host__ __device__ inline int round_up32(int x) { return (x + 31) / 32 * 32; }
 
@@ -47,10 +57,11 @@ __device__ __forceinline__ float pair_other(float x) {
     return __uint_as_float(r[0] ^ r[1] ^ u);
 }
 
-// One pass over the keys of a 1024-key split for the row set (l, g).  NW waves
+// One pass over the keys of a 2048-key split for the row set (l, g).  NW waves
 // each hold one 32-row block of the row set's queries in registers (row rho =
-// t*G + hh reads q[l][t][g*G + hh][:]); K tiles of 128 contiguous keys stream
-// through double-buffered LDS.
+// t*G + hh reads q[l][t][g*G + hh][:]); 16 KB tiles of K stream into a ring of
+// kStages swizzled LDS buffers by direct global->LDS loads, kStages-1 tiles
+// ahead of the MFMAs.
 //   STATS: S^T = K Q^T (one query row per lane): per-lane online (max, sum of
 //          exp2) over its keys, merged with the lane 32 away at the end ->
 //          stats[l][g][split][row] in log2 units.
@@ -58,42 +69,70 @@ __device__ __forceinline__ float pair_other(float x) {
 //          16 rows, the two half-waves added, then a fixed-order sum over the
 //          waves in LDS -> part[l][g][key].
 template <int D, int NW, bool STATS>
-__global__ __launch_bounds__(NW * 64) void score_pass_bf16(
+__global__ __launch_bounds__(NW * 64, score_waves_per_simd<NW>()) void score_pass_bf16(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
     int Hkv, int G, int n_rows, int rows_pad, int n_split, float sl2,
     float2* __restrict__ stats, const float* __restrict__ lse2, const float* __restrict__ q_lse,
     float* __restrict__ part) {
-    constexpr int NT = NW * 64;
+    constexpr int TK = tile_keys<D>();              // keys per tile
+    constexpr int NT = kKeysPerSplit / TK;          // tiles per split
     constexpr int KS = D / 16;
-    constexpr int KSTR = D + 8;
-    constexpr int P = D / 8;
-    constexpr int NB = kTileKeys / 32;
-    constexpr int CHUNKS = kTileKeys * P;          // 16-byte chunks per tile
-    constexpr int CPT = (CHUNKS + NT - 1) / NT;     // chunks per thread
-    constexpr int RING = 4;                         // K fragments read ahead
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kTileKeys * KSTR];
-    __shared__ float colp[2][STATS ? 1 : NW][kTileKeys];
+    constexpr int NB = TK / 32;                     // 32-key MFMA blocks per tile
+    constexpr int ROWB = 2 * D;                     // tile row bytes
+    constexpr int CH = D / 8;                       // 16-byte chunks per row
+    constexpr int RPI = 64 / CH;                    // rows per wave-wide load
+    constexpr int NL = TK / RPI;                    // wave-wide loads per tile (16)
+    constexpr int LPW = NL / NW;                    // loads per tile every wave issues (some one more)
+    constexpr int NI = (NL + NW - 1) / NW;
+    static_assert(LPW >= 1 && kStages == 4 && TK % 64 == 0, "pipeline shape");
+    __shared__ __attribute__((aligned(1024))) uint16_t Ks[kStages][TK * D];
+    __shared__ float colp[2][STATS ? 1 : NW][TK];
+    __shared__ __attribute__((aligned(16))) float lrs[STATS ? 1 : NW][32];
 
     const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, r32 = lane & 31, hf = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, hf = lane >> 5;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
     const int key0 = split * kKeysPerSplit;
-    const int ntile = min(kTilesPerSplit, (T - key0 + kTileKeys - 1) / kTileKeys);
+    const int ntile = min(NT, (T - key0 + TK - 1) / TK);
 
-    u32x4 st[CPT];
-    auto load_tile = [&](int tt) {
-        const int kbase = key0 + tt * kTileKeys;
+    // Tile tt into stage tt % kStages.  Wave w issues loads j = w, w+NW, ...;
+    // lane l of load j fills (row j*RPI + l/CH, chunk l%CH).  Rows past T re-read
+    // row T-1: their logits are masked (STATS) or their sums never stored.
+    const int lrow = lane / CH, pchunk = lane % CH;
+    uint32_t loff[NI];                              // byte offset of this lane's chunk in a tile
 #pragma unroll
-        for (int i = 0; i < CPT; ++i) {
-            const int c = tid + i * NT;
-            const int key = kbase + c / P;
-            st[i] = (c < CHUNKS && key < T) ? *(const u32x4*)(Kg + (size_t)key * D + (c % P) * 8)
-                                            : u32x4{0u, 0u, 0u, 0u};
+    for (int i = 0; i < NI; ++i) {
+        const int row = (w + i * NW) * RPI + lrow;
+        loff[i] = (uint32_t)(row * ROWB + ((pchunk ^ tile_swz<D>(row)) << 4));
+    }
+    auto issue_tile = [&](int tt) {
+        uint16_t* st = Ks[tt % kStages];
+        const int kb = key0 + tt * TK;
+        const char* tb = (const char*)(Kg + (size_t)kb * D);
+        const bool tail = kb + TK > T;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int j = w + i * NW;
+            if (i < LPW || j < NL) {
+                uint32_t o = loff[i];
+                if (tail) {                                  // clamp the row to T-1
+                    const int row = j * RPI + lrow;
+                    o = (uint32_t)((min(kb + row, T - 1) - kb) * ROWB) + (o & (ROWB - 1));
+                }
+                load_lds16(tb + o, st + j * RPI * D);
+            }
         }
     };
-    auto reduce_cols = [&](int tt, bool first_chunk) {   // phase 2: sum over waves
-        const int key = key0 + tt * kTileKeys + tid;
-        if (tid < kTileKeys && key < T) {
+    // Wait for tile tt (rem tiles were issued after it), then barrier.
+    auto wait_tile = [&](int rem) {
+        if (rem >= 2) wait_loads_barrier<2 * LPW>();
+        else if (rem == 1) wait_loads_barrier<LPW>();
+        else wait_loads_barrier<0>();
+    };
+    auto reduce_cols = [&](int tt, bool first_chunk) {   // colsum: fixed-order sum over waves
+        const int key = key0 + tt * TK + tid;
+        if (tid < TK && key < T) {
             float v = 0.f;
 #pragma unroll
             for (int ww = 0; ww < NW; ++ww) v += colp[tt & 1][STATS ? 0 : ww][tid];
@@ -101,9 +140,10 @@ __global__ __launch_bounds__(NW * 64) void score_pass_bf16(
             *dst = first_chunk ? v : *dst + v;
         }
     };
+    // K fragment (tile row 32b + r32, logical chunk 2ks + hf) byte offset.
+    const int k_base = r32 * ROWB | ((hf ^ tile_swz<D>(r32)) << 4);
 
     for (int rc0 = 0; rc0 < rows_pad; rc0 += NW * 32) {
-        // This lane's query fragments (row rho, k-half hf).
         const int rho = rc0 + w * 32 + r32;
         bf16x8 qf[KS];
         if (rho < n_rows) {
@@ -115,92 +155,78 @@ __global__ __launch_bounds__(NW * 64) void score_pass_bf16(
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) qf[ks] = bf16x8{};
         }
-        // Phase 2: log2-sum-exp of the 16 rows this lane accumulates
-        // (rows rc0 + w*32 + 8j + 4hf + i); padding rows get +inf.
-        float lr[16];
+        // Colsum: log2-sum-exp of the wave's 32 rows, kept in LDS (padding rows
+        // get +inf); the lane that accumulates rows 8j + 4hf + i reads
+        // lrs[w][8j + 4hf .. +3] as one 16-byte broadcast.
         if constexpr (!STATS) {
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int row = rc0 + w * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
+            if (lane < 32) {
+                const int row = rc0 + w * 32 + lane;
                 float x = INFINITY;
                 if (row < n_rows) {
                     x = q_lse ? q_lse[((size_t)l * Qn + row / G) * H + g * G + row % G] * kLog2e
                               : lse2[((size_t)l * Hkv + g) * rows_pad + row];
                 }
-                lr[v] = x;
+                lrs[w][lane] = x;
             }
         }
         float m_run = -INFINITY, z_run = 0.f;
 
         __syncthreads();                                // LDS free from the previous row chunk
-        load_tile(0);
+#pragma unroll
+        for (int tt = 0; tt < kStages - 1; ++tt)
+            if (tt < ntile) issue_tile(tt);
         for (int tt = 0; tt < ntile; ++tt) {
-            uint16_t* kb = Ks[tt & 1];
-#pragma unroll
-            for (int i = 0; i < CPT; ++i) {
-                const int c = tid + i * NT;
-                if (c < CHUNKS) *(u32x4*)(kb + (c / P) * KSTR + (c % P) * 8) = st[i];
-            }
-            __syncthreads();
+            wait_tile(min(kStages - 2, ntile - 1 - tt));
             if (!STATS && tt > 0) reduce_cols(tt - 1, rc0 == 0);
-            if (tt + 1 < ntile) load_tile(tt + 1);
-
-            const int kbase = key0 + tt * kTileKeys;
-            // Two 32-key blocks at a time (two independent MFMA chains), K
-            // fragments read RING MFMAs ahead.
+            if (tt + kStages - 1 < ntile) issue_tile(tt + kStages - 1);
+            const char* kt = (const char*)Ks[tt % kStages];
+            const int kbase = key0 + tt * TK;
 #pragma unroll
-            for (int bp = 0; bp < NB / 2; ++bp) {
-                f32x16 acc[2] = {f32x16{}, f32x16{}};
-                const uint16_t* kp = kb + (64 * bp + r32) * KSTR + hf * 8;
-                bf16x8 kf[RING];
+            for (int b = 0; b < NB; ++b) {
+                // 32-key block: KS MFMAs, K fragments read kRing ahead.
+                const char* kp = kt + b * 32 * ROWB;
+                bf16x8 kf[kRing];
 #pragma unroll
-                for (int i = 0; i < RING; ++i) kf[i] = *(const bf16x8*)(kp + (i & 1) * 32 * KSTR + (i >> 1) * 16);
+                for (int i = 0; i < kRing; ++i) kf[i] = *(const bf16x8*)(kp + (k_base ^ (i << 5)));
+                f32x16 acc = f32x16{};
 #pragma unroll
-                for (int sx = 0; sx < 2 * KS; ++sx) {
-                    const int ks = sx >> 1, i = sx & 1;
-                    const bf16x8 cur = kf[sx % RING];
-                    if (sx + RING < 2 * KS) {
-                        const int s2 = sx + RING;
-                        kf[sx % RING] = *(const bf16x8*)(kp + (s2 & 1) * 32 * KSTR + (s2 >> 1) * 16);
-                    }
+                for (int ks = 0; ks < KS; ++ks) {
+                    const bf16x8 cur = kf[ks % kRing];
+                    if (ks + kRing < KS) kf[ks % kRing] = *(const bf16x8*)(kp + (k_base ^ ((ks + kRing) << 5)));
                     if constexpr (STATS)
-                        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[ks], acc[i], 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[ks], acc, 0, 0, 0);
                     else
-                        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], cur, acc[i], 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], cur, acc, 0, 0, 0);
                 }
-                const int kb0 = kbase + 64 * bp;
+                const int kb0 = kbase + 32 * b;
                 if constexpr (STATS) {
-                    // acc[i][v] = S[row r32][key kb0 + 32i + 8(v/4) + 4hf + v%4]
-                    if (kb0 + 64 > T) {
+                    // acc[v] = S[row r32][key kb0 + 8(v/4) + 4hf + v%4]
+                    if (kb0 + 32 > T) {
 #pragma unroll
-                        for (int i = 0; i < 2; ++i)
-#pragma unroll
-                            for (int v = 0; v < 16; ++v)
-                                if (kb0 + 32 * i + 8 * (v >> 2) + 4 * hf + (v & 3) >= T)
-                                    acc[i][v] = -INFINITY;
+                        for (int v = 0; v < 16; ++v)
+                            if (kb0 + 8 * (v >> 2) + 4 * hf + (v & 3) >= T) acc[v] = -INFINITY;
                     }
-                    float mt = fmaxf(acc[0][0], acc[1][0]);
+                    float mt = acc[0];
 #pragma unroll
-                    for (int v = 1; v < 16; ++v) mt = fmaxf(mt, fmaxf(acc[0][v], acc[1][v]));
+                    for (int v = 1; v < 16; ++v) mt = fmaxf(mt, acc[v]);
                     const float m_new = fmaxf(m_run, mt * sl2);
                     const float mref = m_new == -INFINITY ? 0.f : m_new;
                     float z = z_run * fast_exp2(m_run - mref);
 #pragma unroll
-                    for (int i = 0; i < 2; ++i)
-#pragma unroll
-                        for (int v = 0; v < 16; ++v) z += fast_exp2(fmaf(acc[i][v], sl2, -mref));
+                    for (int v = 0; v < 16; ++v) z += fast_exp2(fmaf(acc[v], sl2, -mref));
                     z_run = z;
                     m_run = m_new;
                 } else {
-                    // acc[i][v] = S[row rc0 + w*32 + 8(v/4) + 4hf + v%4][key kb0 + 32i + r32]
+                    // acc[v] = S[row rc0 + w*32 + 8(v/4) + 4hf + v%4][key kb0 + r32]
+                    float cs = 0.f;
 #pragma unroll
-                    for (int i = 0; i < 2; ++i) {
-                        float cs = 0.f;
+                    for (int j = 0; j < 4; ++j) {
+                        const f32x4 lr = *(const f32x4*)&lrs[w][8 * j + 4 * hf];
 #pragma unroll
-                        for (int v = 0; v < 16; ++v) cs += fast_exp2(fmaf(acc[i][v], sl2, -lr[v]));
-                        const float other = pair_other(cs);
-                        if (hf == 0) colp[tt & 1][STATS ? 0 : w][64 * bp + 32 * i + r32] = cs + other;
+                        for (int i = 0; i < 4; ++i) cs += fast_exp2(fmaf(acc[4 * j + i], sl2, -lr[i]));
                     }
+                    const float other = pair_other(cs);
+                    if (hf == 0) colp[tt & 1][w][32 * b + r32] = cs + other;
                 }
             }
         }
@@ -329,39 +355,84 @@ __global__ __launch_bounds__(256) void score_colsum_f32(const float* __restrict_
 
 // ---------------------------------------------------------------- finaliser
 
-__global__ __launch_bounds__(1024) void score_finalize(const float* __restrict__ part, int n_part,
-                                                       int T, float inv_hq,
-                                                       float* __restrict__ scores) {
-    __shared__ float red_lo[16], red_hi[16];
-    const int l = blockIdx.x, tid = threadIdx.x;
-    float* a = scores + (size_t)l * T;
+// Finaliser, two launches over (key block, layer):
+//   score_pool: p_i = (1/(H Qn)) * sum over the n_part partial slices (fixed
+//     order), written to scores, plus each block's (min, max) of p;
+//   score_minmax: every block reduces its layer's block extrema (fixed order)
+//     and rescales its keys to a = (p - min) / (max - min), or 0 when flat.
+constexpr int kFinKeys = 1024;                 // keys per finaliser block (256 threads x 4)
+
+__global__ __launch_bounds__(256) void score_pool(const float* __restrict__ part, int n_part,
+                                                  int T, float inv_hq, float* __restrict__ scores,
+                                                  float2* __restrict__ mm, int n_blk) {
+    __shared__ float red_lo[4], red_hi[4];
+    const int blk = blockIdx.x, l = blockIdx.y, tid = threadIdx.x;
     float lo = INFINITY, hi = -INFINITY;
-    for (int i = tid; i < T; i += 1024) {
-        float p = 0.f;
-        for (int j = 0; j < n_part; ++j) p += part[((size_t)l * n_part + j) * T + i];
-        p *= inv_hq;
-        a[i] = p;
-        lo = fminf(lo, p);
-        hi = fmaxf(hi, p);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int i = blk * kFinKeys + e * 256 + tid;
+        if (i < T) {
+            float p = 0.f;
+            for (int j = 0; j < n_part; ++j) p += part[((size_t)l * n_part + j) * T + i];
+            p *= inv_hq;
+            scores[(size_t)l * T + i] = p;
+            lo = fminf(lo, p);
+            hi = fmaxf(hi, p);
+        }
     }
-    for (int o = 32; o > 0; o >>= 1) {
-        lo = fminf(lo, __shfl_xor(lo, o, 64));
-        hi = fmaxf(hi, __shfl_xor(hi, o, 64));
-    }
+    lo = -wave_max(-lo);
+    hi = wave_max(hi);
     if ((tid & 63) == 0) {
         red_lo[tid >> 6] = lo;
         red_hi[tid >> 6] = hi;
     }
     __syncthreads();
-    lo = red_lo[0];
-    hi = red_hi[0];
-    for (int i = 1; i < 16; ++i) {
-        lo = fminf(lo, red_lo[i]);
-        hi = fmaxf(hi, red_hi[i]);
+    if (tid == 0) {
+        float a = red_lo[0], b = red_hi[0];
+        for (int i = 1; i < 4; ++i) {
+            a = fminf(a, red_lo[i]);
+            b = fmaxf(b, red_hi[i]);
+        }
+        mm[(size_t)l * n_blk + blk] = make_float2(a, b);
     }
+}
+
+__global__ __launch_bounds__(256) void score_minmax(const float2* __restrict__ mm, int n_blk, int T,
+                                                    float* __restrict__ scores) {
+    __shared__ float red_lo[4], red_hi[4];
+    const int blk = blockIdx.x, l = blockIdx.y, tid = threadIdx.x;
+    float lo = INFINITY, hi = -INFINITY;
+    for (int b = tid; b < n_blk; b += 256) {
+        const float2 v = mm[(size_t)l * n_blk + b];
+        lo = fminf(lo, v.x);
+        hi = fmaxf(hi, v.y);
+    }
+    lo = -wave_max(-lo);
+    hi = wave_max(hi);
+    if ((tid & 63) == 0) {
+        red_lo[tid >> 6] = lo;
+        red_hi[tid >> 6] = hi;
+    }
+    __syncthreads();
+    lo = fminf(fminf(red_lo[0], red_lo[1]), fminf(red_lo[2], red_lo[3]));
+    hi = fmaxf(fmaxf(red_hi[0], red_hi[1]), fmaxf(red_hi[2], red_hi[3]));
     const bool flat = !(hi > lo);
     const float span = hi - lo;
-    for (int i = tid; i < T; i += 1024) a[i] = flat ? 0.f : (a[i] - lo) / span;
+    float* a = scores + (size_t)l * T;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int i = blk * kFinKeys + e * 256 + tid;
+        if (i < T) a[i] = flat ? 0.f : (a[i] - lo) / span;
+    }
+}
+
+void launch_finalize(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws, float* scores,
+                     hipStream_t st) {
+    const dim3 grid(w.n_blk, p.L);
+    float2* mm = (float2*)(ws + w.mm_off);
+    hipLaunchKernelGGL(score_pool, grid, dim3(256), 0, st, (const float*)(ws + w.part_off), w.n_part,
+                       p.T_c, 1.0f / ((float)p.H * (float)p.n_query), scores, mm, w.n_blk);
+    hipLaunchKernelGGL(score_minmax, grid, dim3(256), 0, st, (const float2*)mm, w.n_blk, p.T_c, scores);
 }
 
 template <int D, int NW>
@@ -398,8 +469,7 @@ hipError_t launch_score_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, 
     if (nrb <= 4) launch_passes_bf16<D, 4>(p, w, ws, st, sl2);
     else if (nrb <= 8 || nrb > kMaxWaves) launch_passes_bf16<D, 8>(p, w, ws, st, sl2);
     else launch_passes_bf16<D, kMaxWaves>(p, w, ws, st, sl2);
-    hipLaunchKernelGGL(score_finalize, dim3(p.L), dim3(1024), 0, st, (const float*)(ws + w.part_off),
-                       w.n_part, p.T_c, 1.0f / ((float)p.H * (float)p.n_query), scores);
+    launch_finalize(p, w, ws, scores, st);
     return hipGetLastError();
 }
 
@@ -417,8 +487,7 @@ hipError_t launch_score_f32(const relaxkv_problem& p, const ScoreWorkspace& w, c
     hipLaunchKernelGGL(score_colsum_f32<D>, dim3((p.T_c + 255) / 256, p.L), dim3(256), 0, st, q,
                        kc, p.T_c, p.n_query, p.H, p.H_kv, G, w.rows_pad, scale, lse, p.q_lse,
                        part);
-    hipLaunchKernelGGL(score_finalize, dim3(p.L), dim3(1024), 0, st, part, w.n_part, p.T_c,
-                       1.0f / ((float)p.H * (float)p.n_query), scores);
+    launch_finalize(p, w, ws, scores, st);
     return hipGetLastError();
 }
 
@@ -438,6 +507,9 @@ ScoreWorkspace score_workspace_layout(const relaxkv_problem& p) {
     if (bf) off += al((size_t)p.L * p.H_kv * w.n_split * w.rows_pad * sizeof(float2));
     w.lse_off = off;
     off += al((size_t)p.L * p.H_kv * w.rows_pad * sizeof(float));
+    w.n_blk = (p.T_c + kFinKeys - 1) / kFinKeys;
+    w.mm_off = off;
+    off += al((size_t)p.L * w.n_blk * sizeof(float2));
     w.total = off;
     return w;
 }
