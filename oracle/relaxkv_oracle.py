@@ -25,6 +25,12 @@ with Sparse Context Attention for Efficient KV Cache Reuse"):
                       ``mode="full"``.
 * ``update_cache`` -- Sec. 3.4 cache-update semantics, Algorithm 1 update step:
                       fresh rows of R_l overwrite their cache positions.
+* ``global_scores``, ``global_target_count``, ``select_global``,
+  ``build_sets_global`` -- the matched-target variants: RelaxKV^G (Sec. 4.1
+                      comparison setup; App. A.3 table "Controlled
+                      configurations") keeps a global target set P for every
+                      layer with the context C_l(p); the global repair target
+                      sweep (App. B equation) ranks g_i = (1/L) sum_l a_{l,i}.
 
 Readings where the paper is silent (each also listed in the design notes):
 
@@ -38,7 +44,10 @@ Readings where the paper is silent (each also listed in the design notes):
   clamped to [1, T_c];
 * equal scores are ordered by ascending position; -0.0 equals +0.0; a NaN
   score is an error;
-* layers are 0-based, positions are context positions 0..T_c-1 only.
+* layers are 0-based, positions are context positions 0..T_c-1 only;
+* a global target p need not lie in U; its context U cap {j <= p} may then be
+  empty, and attention over an empty context is the empty sum: O = 0 and
+  log-sum-exp = -inf.
 
 Pins: every function is checked in ``tests/test_oracle_pins.py`` against
 something other than itself (closed forms, a hand-worked example, brute force
@@ -202,6 +211,76 @@ def build_sets(anchors, T_c):
 
 
 # ----------------------------------------------------------------------------
+# Matched-target variants: RelaxKV^G (App. A.3 table) and the global repair
+# target sweep (App. B equation).
+# ----------------------------------------------------------------------------
+
+def global_scores(a):
+    """g_i = (1/L) sum_l a_{l,i}: the layer mean of the normalised scores (App. B)."""
+    a = np.asarray(a, dtype=np.float64)
+    return a.sum(axis=0) / a.shape[0]
+
+
+def global_target_count(ratio, T_c, n_union):
+    """|P_{r_g}| = min(floor(r_g T_c), |U|) (App. B equation)."""
+    ratio = float(ratio)
+    if not np.isfinite(ratio) or ratio < 0.0 or ratio > 1.0:
+        raise ValueError("target ratio must be a finite number in [0, 1]")
+    return min(int(np.floor(ratio * T_c)), int(n_union))
+
+
+def select_global(g, n_targets):
+    """P = TopK_i(g_i, n_targets), lowest position first among equal g,
+    returned ascending (App. B equation)."""
+    g = np.asarray(g, dtype=np.float64)
+    if n_targets == 0:
+        return np.zeros(0, dtype=np.int64)
+    return select(g[None, :], int(n_targets))[0]
+
+
+def build_sets_global(anchors, T_c, P):
+    """Sets of a matched-target variant: the context is still the union U of
+    the layer-wise anchors, but every layer repairs the same global target
+    list P (sorted, distinct positions).
+
+    R_l = P for every l; the compact limit of a target p is
+    |U cap {j <= p}| - 1, which is -1 (empty context) when p precedes every
+    union position; src[l][c] is the rank of U[c] in P or -1; h_i = L - 1 for
+    targets (active at every layer) and -1 otherwise.
+    """
+    anchors = np.asarray(anchors, dtype=np.int64)
+    P = np.asarray(P, dtype=np.int64)
+    if P.ndim != 1 or (len(P) > 0 and (P.min() < 0 or P.max() >= T_c)):
+        raise ValueError("targets must be positions in [0, T_c)")
+    if np.any(np.diff(P) <= 0):
+        raise ValueError("targets must be strictly ascending")
+    L = anchors.shape[0]
+    in_union = np.zeros(T_c, dtype=bool)
+    for l in range(L):
+        in_union[anchors[l]] = True
+    U = np.flatnonzero(in_union)
+    cidx = np.full(T_c, -1, dtype=np.int64)
+    cidx[U] = np.arange(len(U))
+    h = np.full(T_c, -1, dtype=np.int64)
+    h[P] = L - 1
+    # |U cap {j <= p}| for every target, counted directly.
+    n_le = np.array([int(np.count_nonzero(U <= p)) for p in P], dtype=np.int64)
+    u = n_le - 1
+    rank = np.full(T_c, -1, dtype=np.int64)
+    rank[P] = np.arange(len(P))
+    s_l = rank[U]
+    R, R_u, src = [], [], []
+    for _ in range(L):
+        R.append(P.copy())
+        R_u.append(u.copy())
+        src.append(s_l.copy())
+    edges = np.full(L, int(np.sum(n_le)), dtype=np.int64)
+    edges_full = np.full(L, int(np.sum(P + 1)), dtype=np.int64)
+    return Sets(T_c=T_c, k=anchors.shape[1], anchors=anchors, h=h, U=U, cidx=cidx,
+                R=R, R_u=R_u, src=src, edges=edges, edges_full=edges_full)
+
+
+# ----------------------------------------------------------------------------
 # Sparse-context attention: Sec. 3.3, Sec. 3.4 equation, App. A.2.
 # ----------------------------------------------------------------------------
 
@@ -261,6 +340,9 @@ def sparse_attn(layer, sets, q_new, k_new, v_new, k_cache_l, v_cache_l,
     for n, t in enumerate(ts):
         p = R_l[t]
         m = int(np.searchsorted(ctx_all, p, side="right"))   # |{j in ctx : j <= p}|
+        if m == 0:                       # empty context: the empty sum
+            lse[n, :] = -np.inf
+            continue
         for h in range(H):
             g = h // G
             s = sigma * (Kt[g, :m, :] @ q_new[t, h])           # [m]

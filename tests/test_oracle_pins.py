@@ -430,3 +430,153 @@ def test_update_cache_then_full_prefix_attention_reads_fresh_rows():
     # positions outside R_l keep their naive values
     outside = np.setdiff1d(np.arange(T), s.R[l])
     assert np.array_equal(k2[:, outside], kc[:, outside])
+
+
+# ----------------------------------------------------------------------------
+# matched-target variants: RelaxKV^G and the global repair target sweep
+# ----------------------------------------------------------------------------
+
+def test_global_scores_closed_form_and_loops():
+    from oracle import global_scores
+    a = np.array([[0.0, 1.0, 0.5, 0.25], [1.0, 0.0, 0.5, 0.75]])
+    assert global_scores(a).tolist() == [0.5, 0.5, 0.5, 0.5]
+    rng = np.random.default_rng(21)
+    a = rng.random((7, 31))
+    g = global_scores(a)
+    for i in range(31):
+        assert g[i] == pytest.approx(math.fsum(a[l, i] for l in range(7)) / 7, abs=1e-15)
+
+
+@pytest.mark.parametrize("r,T,nU,n", [
+    (0.2, 1000, 500, 200), (0.2, 1000, 150, 150), (0.15, 1001, 999, 150),   # floor(150.15)
+    (0.0, 64, 10, 0), (1.0, 64, 40, 40), (0.7, 10, 10, 7), (0.05, 19, 19, 0),
+])
+def test_global_target_count_floor_and_cap(r, T, nU, n):
+    from oracle import global_target_count
+    assert global_target_count(r, T, nU) == n
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.integers(1, 50), st.integers(0, 2**31 - 1), st.data())
+def test_select_global_brute_force_with_ties(T, seed, data):
+    from oracle import select_global
+    rng = np.random.default_rng(seed)
+    g = rng.integers(0, 4, size=T) / 4.0                      # many equal values
+    n = data.draw(st.integers(0, T))
+    order = sorted(range(T), key=lambda i: (-g[i], i))        # larger g first, then lower i
+    assert select_global(g, n).tolist() == sorted(order[:n])
+
+
+def test_build_sets_global_equals_relaxkv_sets_for_identical_layers():
+    # When every layer selects the same anchors S, RelaxKV's targets are R_l = S = U
+    # for every layer, which is the matched-target variant with P = S.
+    from oracle import build_sets_global
+    rng = np.random.default_rng(22)
+    L, T, k = 4, 50, 9
+    S1 = np.sort(rng.choice(T, size=k, replace=False))
+    S = np.tile(S1, (L, 1))
+    a, b = build_sets(S, T), build_sets_global(S, T, S1)
+    assert a.U.tolist() == b.U.tolist() and a.h.tolist() == b.h.tolist()
+    assert a.cidx.tolist() == b.cidx.tolist()
+    for l in range(L):
+        for f in ("R", "R_u", "src"):
+            assert getattr(a, f)[l].tolist() == getattr(b, f)[l].tolist()
+    assert a.edges.tolist() == b.edges.tolist() and a.edges_full.tolist() == b.edges_full.tolist()
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.integers(1, 4), st.integers(1, 40), st.integers(0, 2**31 - 1), st.data())
+def test_build_sets_global_brute_force(L, T, seed, data):
+    from oracle import build_sets_global
+    rng = np.random.default_rng(seed)
+    k = data.draw(st.integers(1, T))
+    S = _random_anchors(rng, L, T, k)
+    n = data.draw(st.integers(0, T))
+    P = np.sort(rng.choice(T, size=n, replace=False))
+    s = build_sets_global(S, T, P)
+    U = sorted(set(int(x) for row in S for x in row))
+    assert s.U.tolist() == U
+    for l in range(L):
+        assert s.R[l].tolist() == P.tolist()
+        for t, p in enumerate(P.tolist()):
+            assert s.R_u[l][t] == sum(1 for j in U if j <= p) - 1     # -1: empty context
+        for c, pos in enumerate(U):
+            assert s.src[l][c] == (P.tolist().index(pos) if pos in P.tolist() else -1)
+        assert s.edges[l] == sum(sum(1 for j in U if j <= p) for p in P.tolist())
+        assert s.edges_full[l] == sum(p + 1 for p in P.tolist())
+    for i in range(T):
+        assert s.h[i] == (L - 1 if i in P.tolist() else -1)
+    with pytest.raises(ValueError):
+        build_sets_global(S, T, np.array([1, 1]) if T > 1 else np.array([0, 0]))
+
+
+def _brute_attention_global(P, U, T, qn, kn, vn, kc, vc, sigma, mode):
+    """Dense masked attention for a global target list: target p sees
+    j in U with j <= p (union) or j <= p (full); fresh row iff j in P."""
+    rank = {p: t for t, p in enumerate(P)}
+    H, d = qn.shape[1], qn.shape[2]
+    G = H // kc.shape[0]
+    O = np.zeros((len(P), H, d))
+    lse = np.full((len(P), H), -np.inf)
+    for t, p in enumerate(P):
+        for hh in range(H):
+            g = hh // G
+            terms = []
+            for j in range(T):
+                if not ((j in U and j <= p) if mode == "union" else (j <= p)):
+                    continue
+                kj = kn[rank[j], g] if j in rank else kc[g, j]
+                vj = vn[rank[j], g] if j in rank else vc[g, j]
+                terms.append((sigma * float(np.dot(qn[t, hh], kj)), vj))
+            if not terms:
+                continue                                  # empty sum: O = 0, lse = -inf
+            m = max(x for x, _ in terms)
+            w = [math.exp(x - m) for x, _ in terms]
+            z = math.fsum(w)
+            O[t, hh] = sum(wi * vj for wi, (_, vj) in zip(w, terms)) / z
+            lse[t, hh] = m + math.log(z)
+    return O, lse
+
+
+@pytest.mark.parametrize("seed,mode", [(0, "union"), (1, "full"), (2, "union")])
+def test_attention_global_targets_brute_force(seed, mode):
+    from oracle import build_sets_global
+    rng = np.random.default_rng(30 + seed)
+    L, T, H, H_kv, d = 3, 36, 4, 2, 8
+    S = 1 + _random_anchors(rng, L, T - 1, 5)          # position 0 is never in U
+    U = sorted(set(int(x) for row in S for x in row))
+    # targets inside and outside U, including position 0 (empty context)
+    P = sorted(set([0] + rng.choice(T, size=10, replace=False).tolist()))
+    s = build_sets_global(S, T, np.array(P))
+    assert s.R_u[0][0] == -1
+    n = len(P)
+    qn = rng.standard_normal((n, H, d))
+    kn = rng.standard_normal((n, H_kv, d))
+    vn = rng.standard_normal((n, H_kv, d))
+    kc = rng.standard_normal((H_kv, T, d))
+    vc = rng.standard_normal((H_kv, T, d))
+    for l in range(L):
+        O, lse = sparse_attn(l, s, qn, kn, vn, kc, vc, mode=mode)
+        Ob, lseb = _brute_attention_global(P, set(U), T, qn, kn, vn, kc, vc, 1 / math.sqrt(d), mode)
+        np.testing.assert_allclose(O, Ob, atol=1e-12)
+        np.testing.assert_array_equal(np.isinf(lse), np.isinf(lseb))
+        fin = np.isfinite(lseb)
+        np.testing.assert_allclose(lse[fin], lseb[fin], atol=1e-12)
+
+
+def test_attention_empty_context_is_empty_sum():
+    from oracle import build_sets_global
+    T, H, H_kv, d = 10, 2, 1, 4
+    S = np.array([[4, 7], [5, 7]])                 # U = {4, 5, 7}
+    s = build_sets_global(S, T, np.array([1, 3, 6]))
+    assert s.R_u[0].tolist() == [-1, -1, 1]
+    rng = np.random.default_rng(5)
+    qn, kn, vn = (rng.standard_normal((3, hh, d)) for hh in (H, H_kv, H_kv))
+    kc, vc = (rng.standard_normal((H_kv, T, d)) for _ in range(2))
+    O, lse = sparse_attn(0, s, qn, kn, vn, kc, vc)
+    assert np.all(O[:2] == 0.0) and np.all(lse[:2] == -np.inf)
+    # target 6 sees positions 4 and 5 (cached rows: neither is a target)
+    for hh in range(H):
+        x = kc[0, [4, 5]] @ qn[2, hh] / math.sqrt(d)
+        w = np.exp(x - x.max())
+        np.testing.assert_allclose(O[2, hh], (w / w.sum()) @ vc[0, [4, 5]], atol=1e-13)
