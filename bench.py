@@ -165,6 +165,54 @@ def time_cache_update(b: Bench, reps=3):
             "gbs": nbytes / (ms * 1e-3) / 1e9}
 
 
+def time_matched_targets(b: Bench, target_ratio=0.2, reps=2):
+    """Global repair target sweep (App. B) on the same cache and anchors:
+    P = TopK(g, min(floor(r_g T_c), |U|)) with g the layer mean of the scores,
+    R_l = P at every layer with the union context (RelaxKV^G's matched-target
+    setup).  Times select_global + build_sets_global and the 40 attention
+    launches; the RelaxKV sets are rebuilt afterwards."""
+    w = b.w
+    req, sets = b.req, b.sets
+    g = torch.empty(w.T_c, dtype=torch.float32, device="cuda")
+    P = torch.empty(w.T_c, dtype=torch.int32, device="cuda")
+    n = torch.empty(1, dtype=torch.int32, device="cuda")
+    req.select_global(b.scores, target_ratio, sets, g, P, n)
+    req.build_sets_global(sets, P, n)
+    counts, edges = sets.counts_to_host()
+    nP = counts[1]
+    tgt = P[:nP].cpu().numpy()
+    fresh = []
+    for l in range(w.L):
+        qn, kn, vn = synth.make_fresh_layer(w, l, b.kc[l], b.vc[l], "cuda")
+        fresh.append(tuple(synth.gather_rows(t, tgt) for t in (qn, kn, vn)))
+        del qn, kn, vn
+    out = torch.empty(nP, w.H, w.d, dtype=b.q.dtype, device="cuda")
+    mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    ms_sel, ms_attn = [], []
+    for i in range(reps + 1):
+        e0, e1, e2 = mk(), mk(), mk()
+        e0.record()
+        req.select_global(b.scores, target_ratio, sets, g, P, n)
+        req.build_sets_global(sets, P, n)
+        e1.record()
+        for l in range(w.L):
+            req.sparse_attn(sets, l, *fresh[l], out, None)
+        e2.record()
+        torch.cuda.synchronize()
+        if i:
+            ms_sel.append(e0.elapsed_time(e1))
+            ms_attn.append(e1.elapsed_time(e2))
+    del fresh
+    req.build_sets(sets)                     # back to RelaxKV's own targets
+    torch.cuda.synchronize()
+    E = float(sum(edges[:w.L]))
+    attn_ms = float(np.mean(ms_attn))
+    return {"target_ratio": target_ratio, "n_targets": nP, "union": counts[0],
+            "select_and_sets_ms": float(np.mean(ms_sel)), "attn_ms_all_layers": attn_ms,
+            "attn_tflops": 4.0 * w.H * w.d * E / (attn_ms * 1e-3) / 1e12,
+            "edges": E, "edges_full_prefix": float(sum(edges[w.L:]))}
+
+
 def time_scoring_supplied_lse(b: Bench, reps=5):
     """Time relaxkv_score in its one-pass mode: each query row's log-sum-exp is
     supplied, as the query's own forward pass would produce it (computed here
@@ -314,6 +362,7 @@ def main():
                      "avg_launch_ms": r["attn_launch_ms_avg"]},
     }
     res["cache_update"] = time_cache_update(b)
+    res["matched_targets"] = time_matched_targets(b)
     if args.control:
         rc = b.timed(args.steps, args.warmup, mode=relaxkv.CONTEXT_FULL)
         res["control"] = {"attn_ms_full_prefix": rc["attn_ms_total"],

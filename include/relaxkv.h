@@ -14,6 +14,10 @@
  *   relaxkv_sparse_attn attention of R_l over C_l(p) = U cap {j <= p}
  *                       with the mixed fresh/cached K~, V~ rule          (Sec. 3.3, 3.4, App. A.2)
  *
+ * plus the cache update of the repaired rows (relaxkv_update_cache, Sec. 3.4)
+ * and the matched-target variants, where one global target list replaces R_l
+ * (relaxkv_select_global, relaxkv_build_sets_global; Sec. 4.1, App. A.3, App. B).
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Device pointers are HIP device memory of the current device; host
@@ -103,10 +107,17 @@ typedef struct relaxkv_problem {
  *   rank     [L][T_c]      rank[l*T_c + j] = rank of position j within R_l, or -1 when j is
  *                          not an active target of layer l (position-indexed view of src).
  *   counts   [L+2]         counts[0] = |U|; counts[1+l] = |R_l|; counts[L+1] = error
- *                          word (nonzero when a NaN score reached relaxkv_select).
+ *                          word: bit 0 when a NaN score reached relaxkv_select or
+ *                          relaxkv_select_global, bit 1 when relaxkv_build_sets_global
+ *                          got an invalid target list (cleared by relaxkv_select).
  *   edges    [2L]          edges[l] = sum_{p in R_l} |C_l(p)| (App. A.2 edge count);
  *                          edges[L+l] = sum_{p in R_l} (p+1), the full-prefix count.
  *   k        the anchor budget k = max(1, round(r T_c)), computed on the host.
+ *   global_targets  host flag: 0 after relaxkv_sets_bind and relaxkv_build_sets
+ *                   (targets R_l of RelaxKV, |R_l| <= min(T_c, (L-l) k)), 1 after
+ *                   relaxkv_build_sets_global (one target list for every layer,
+ *                   |R_l| <= T_c); the attention and cache-update calls size their
+ *                   grids from it.
  */
 typedef struct relaxkv_sets {
     int32_t L, T_c, k;
@@ -121,6 +132,7 @@ typedef struct relaxkv_sets {
     int32_t* rank;
     int32_t* counts;
     int64_t* edges;
+    int32_t global_targets;
 } relaxkv_sets;
 
 /* Text of a status code (static storage). */
@@ -178,10 +190,50 @@ relaxkv_status relaxkv_select(const relaxkv_problem* p, const float* scores,
  *   h_i = max{l : i in S_l},  U = union_l S_l,  R_l = {i in U : h_i >= l},
  * the compact index of every position in U, the per-layer source map src, the
  * CSR lists R_idx/R_u, counts and edge counts.  Reads s->anchors (ascending
- * rows, entries in [0, T_c)); writes every other array of `s`.
+ * rows, entries in [0, T_c)); writes every other array of `s` and sets
+ * s->global_targets = 0.
  */
-relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, const relaxkv_sets* s,
-                                  void* stream);
+relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, relaxkv_sets* s, void* stream);
+
+/*
+ * Global repair targets of the target-capacity sweep (App. B equation):
+ *   g_i = (1/L) sum_l a_{l,i},   P = TopK_i(g_i, min(floor(r_g T_c), |U|)),
+ * larger g first, equal g to the lower position, P written ascending.
+ *   scores        device [L][T_c] float32: a_{l,i} from relaxkv_score.
+ *   target_ratio  r_g, a finite number in [0, 1] (floor(r_g T_c) in double).
+ *   s             sets after relaxkv_build_sets: |U| is read from s->counts[0]
+ *                 on the device.
+ *   g             device out [T_c] float32: g_i (float32 sum over layers in layer
+ *                 order, then divided by L).
+ *   targets       device out [T_c] int32: P in entries 0 .. |P|-1.
+ *   n_targets     device out [1] int32: |P| (0 when floor(r_g T_c) = 0).
+ * A NaN in g sets bit 0 of the error word of s.
+ */
+relaxkv_status relaxkv_select_global(const relaxkv_problem* p, const float* scores,
+                                     double target_ratio, const relaxkv_sets* s, float* g,
+                                     int32_t* targets, int32_t* n_targets, void* stream);
+
+/*
+ * Sets of the matched-target variants: RelaxKV^G (Sec. 4.1; App. A.3 table
+ * "Controlled configurations") and the global repair target sweep (App. B).
+ * The context is still the union U of the layer-wise anchors in s->anchors,
+ * but every layer repairs the same global target list P:
+ *   R_l = P for every l,  C_l(p) = U cap {j <= p},  K~/V~ fresh exactly for j in P.
+ * A target need not lie in U: its compact limit R_u = |U cap {j <= p}| - 1 is
+ * -1 when no union position precedes it, and relaxkv_sparse_attn returns the
+ * empty sum (O = 0, lse = -inf) for it in the union context.  h_i = L-1 for
+ * targets (active at every layer), -1 otherwise; U, cidx as in
+ * relaxkv_build_sets.
+ *   targets    device [T_c] int32: P, strictly ascending positions in [0, T_c).
+ *   n_targets  device [1] int32: |P| in [0, T_c].
+ * A list that is not strictly ascending within [0, T_c), or a count outside
+ * [0, T_c], sets bit 1 of the error word (relaxkv_counts_to_host then returns
+ * RELAXKV_EINVAL); the arrays are then unspecified but every index in them is
+ * in range.  Sets s->global_targets = 1.
+ */
+relaxkv_status relaxkv_build_sets_global(const relaxkv_problem* p, relaxkv_sets* s,
+                                         const int32_t* targets, const int32_t* n_targets,
+                                         void* stream);
 
 /*
  * Sparse-context causal attention of layer `layer` (Sec. 3.3-3.4, App. A.2;
@@ -198,7 +250,9 @@ relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, const relaxkv_sets* 
  *   out      device out [|R_l|][H][d] dtype: attention output before o_proj.
  *   lse_out  optional device out [|R_l|][H] float32: natural-log normaliser.
  * |R_l| is read on the device from s->counts; the host needs no count.  The
- * naive cache of the layer is read from p->k_cache / p->v_cache.
+ * naive cache of the layer is read from p->k_cache / p->v_cache.  A target
+ * whose context is empty (only with relaxkv_build_sets_global, union context)
+ * gets O = 0 and lse = -inf.
  */
 relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets* s,
                                    int32_t layer, const void* q_new, const void* k_new,
@@ -227,7 +281,8 @@ relaxkv_status relaxkv_update_cache(const relaxkv_problem* p, const relaxkv_sets
  * Synchronising.  Copies s->counts ([L+2] int32) to host_counts and, when
  * host_edges is not NULL, s->edges ([2L] int64) to host_edges, after all work
  * queued on `stream`.  Returns RELAXKV_EINVAL when the device error word is
- * set (a NaN score reached relaxkv_select), RELAXKV_EDEVICE on a HIP error.
+ * set (a NaN score, or an invalid global target list), RELAXKV_EDEVICE on a HIP
+ * error.
  */
 relaxkv_status relaxkv_counts_to_host(const relaxkv_sets* s, int32_t* host_counts,
                                       int64_t* host_edges, void* stream);

@@ -117,8 +117,11 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
     const int t1 = min(t0 + a.BT, nR);
     const int off = a.R_off[a.layer];
     const int32_t* lim_of = FULL ? a.R_idx + off : a.R_u + off;
+    // Limits are compact indices (union) or positions (full prefix).  A global
+    // target that precedes every union position has limit -1 (empty context):
+    // its row masks every key and is written as the empty sum at the end.
     const int cmin = lim_of[t0];
-    const int cmax = lim_of[t1 - 1];
+    const int cmax = max(lim_of[t1 - 1], 0);
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r32 = lane & 31, hf = lane >> 5;
@@ -145,7 +148,7 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
         for (int ks = 0; ks < KS; ++ks) qf[rb][ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[rb][db] = f32x16{};
-        m_run[rb] = -INFINITY;
+        m_run[rb] = lim[rb] < 0 ? 0.f : -INFINITY;     // empty context: every p is exp2(-inf) = 0
         l_run[rb] = 0.f;
     }
 
@@ -357,7 +360,8 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
     for (int rb = 0; rb < RB; ++rb) {
         const float l_tot = pair_sum(l_run[rb]);
         if (!valid[rb]) continue;
-        const float inv = 1.0f / l_tot;
+        const bool empty = lim[rb] < 0;
+        const float inv = empty ? 0.f : 1.0f / l_tot;
         uint16_t* out = (uint16_t*)a.out + ((size_t)t_of[rb] * a.H + head_of[rb]) * D;
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
@@ -372,7 +376,8 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
             }
         }
         if (a.lse && hf == 0)
-            a.lse[(size_t)t_of[rb] * a.H + head_of[rb]] = (m_run[rb] + __log2f(l_tot)) * kLn2;
+            a.lse[(size_t)t_of[rb] * a.H + head_of[rb]] =
+                empty ? -INFINITY : (m_run[rb] + __log2f(l_tot)) * kLn2;
     }
 }
 
@@ -389,6 +394,12 @@ __global__ __launch_bounds__(64) void attn_f32(AttnArgs a) {
     const int g = head / a.G;
     const int off = a.R_off[a.layer];
     const int lim = FULL ? a.R_idx[off + t] : a.R_u[off + t];
+    if (lim < 0) {                                     // empty context: the empty sum
+        float* out = (float*)a.out + ((size_t)t * a.H + head) * D;
+        for (int e = lane; e < D; e += 64) out[e] = 0.f;
+        if (a.lse && lane == 0) a.lse[(size_t)t * a.H + head] = -INFINITY;
+        return;
+    }
     const float* qn = (const float*)a.q_new;
     const float* kn = (const float*)a.k_new;
     const float* vn = (const float*)a.v_new;
@@ -482,9 +493,10 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.layer = layer;
     a.BT = bf16 ? kNW * kRB * 32 / a.G : 1;
     a.scale = p.softmax_scale > 0.f ? p.softmax_scale : 1.0f / sqrtf((float)p.d);
-    // |R_l| <= |union of S_l' for l' >= l| <= min(T_c, (L - l) k); the device
-    // count decides which workgroups run.
-    const long kb = (long)(p.L - layer) * s.k;
+    // |R_l| <= |union of S_l' for l' >= l| <= min(T_c, (L - l) k) for RelaxKV's
+    // targets, <= T_c for a global target list; the device count decides which
+    // workgroups run.
+    const long kb = s.global_targets ? (long)p.T_c : (long)(p.L - layer) * s.k;
     const int n_bound = (int)(kb < p.T_c ? kb : p.T_c);
     const bool full = context_mode == RELAXKV_CONTEXT_FULL;
     if (p.d == 128) {

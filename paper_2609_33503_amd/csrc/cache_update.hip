@@ -5,7 +5,8 @@
 // One pass of 16-byte copies: thread -> (target t, KV head g, 16-byte part), so
 // consecutive threads read consecutive bytes of the fresh rows and write whole
 // d-long rows of the cache.  |R_l| is read on the device; the grid is sized from
-// the host bound |R_l| <= min(T_c, (L - l) k) and surplus threads exit.
+// the host bound |R_l| <= min(T_c, (L - l) k) (T_c for a global target list)
+// and surplus threads exit.
 
 #include "dev_common.h"
 #include "internal.h"
@@ -43,7 +44,7 @@ hipError_t launch_update_cache(const relaxkv_problem& p, const relaxkv_sets& s, 
     const size_t layer_bytes = (size_t)p.H_kv * p.T_c * p.d * esz;
     u32x4* kc = (u32x4*)((char*)k_cache + (size_t)layer * layer_bytes);
     u32x4* vc = (u32x4*)((char*)v_cache + (size_t)layer * layer_bytes);
-    const long kb = (long)(p.L - layer) * s.k;
+    const long kb = s.global_targets ? (long)p.T_c : (long)(p.L - layer) * s.k;
     const long n_bound = (kb < p.T_c ? kb : p.T_c) * (long)p.H_kv * parts;
     const long blocks = (n_bound + 255) / 256;
     hipLaunchKernelGGL(update_cache_rows, dim3((unsigned)(blocks < 8192 ? blocks : 8192)),

@@ -29,6 +29,12 @@ hipError_t launch_score(const relaxkv_problem& p, const ScoreWorkspace& w, char*
                         float* scores, hipStream_t st);
 hipError_t launch_select(const relaxkv_problem& p, const float* scores,
                          const relaxkv_sets& s, hipStream_t st);
+hipError_t launch_select_global(const relaxkv_problem& p, const float* scores, int k_target,
+                                const relaxkv_sets& s, float* g, int32_t* targets,
+                                int32_t* n_targets, hipStream_t st);
+hipError_t launch_build_sets_global(const relaxkv_problem& p, const relaxkv_sets& s,
+                                    const int32_t* targets, const int32_t* n_targets,
+                                    hipStream_t st);
 hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s,
                              hipStream_t st);
 hipError_t launch_update_cache(const relaxkv_problem& p, const relaxkv_sets& s, int layer,

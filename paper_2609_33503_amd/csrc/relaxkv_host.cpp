@@ -2,6 +2,7 @@
 // Nothing here allocates device memory; every buffer belongs to the caller.
 
 #include <math.h>
+#include <stdint.h>
 #include <string.h>
 
 #include "internal.h"
@@ -17,7 +18,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 bool dims_ok(const relaxkv_problem* p) {
     return p->L >= 1 && p->L <= RELAXKV_MAX_LAYERS && p->T_c >= 1 && p->T_c <= RELAXKV_MAX_TC &&
            p->n_query >= 1 && p->n_query <= 4096 && p->H >= 1 && p->H <= 1024 &&
-           p->H_kv >= 1 && p->H % p->H_kv == 0;
+           p->H_kv >= 1 && p->H % p->H_kv == 0 &&
+           (int64_t)p->L * p->T_c <= INT32_MAX;          // CSR offsets over layers are int32
 }
 
 // Byte sizes of the set arrays, in carving order.
@@ -126,6 +128,7 @@ relaxkv_status relaxkv_sets_bind(const relaxkv_problem* p, void* dev_buf, size_t
     s.rank = (int32_t*)b; b += l.rank;
     s.counts = (int32_t*)b; b += l.counts;
     s.edges = (int64_t*)b;
+    s.global_targets = 0;
     *out = s;
     return RELAXKV_OK;
 }
@@ -148,12 +151,37 @@ relaxkv_status relaxkv_select(const relaxkv_problem* p, const float* scores,
     return from_hip(launch_select(*p, scores, *s, (hipStream_t)stream));
 }
 
-relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, const relaxkv_sets* s,
-                                  void* stream) {
+relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, relaxkv_sets* s, void* stream) {
     relaxkv_status st = relaxkv_validate(p);
     if (st != RELAXKV_OK) return st;
     if (!sets_match(p, s)) return RELAXKV_EINVAL;
-    return from_hip(launch_build_sets(*p, *s, (hipStream_t)stream));
+    st = from_hip(launch_build_sets(*p, *s, (hipStream_t)stream));
+    if (st == RELAXKV_OK) s->global_targets = 0;
+    return st;
+}
+
+relaxkv_status relaxkv_select_global(const relaxkv_problem* p, const float* scores,
+                                     double target_ratio, const relaxkv_sets* s, float* g,
+                                     int32_t* targets, int32_t* n_targets, void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!scores || !g || !targets || !n_targets || !sets_match(p, s)) return RELAXKV_EINVAL;
+    if (!isfinite(target_ratio) || target_ratio < 0.0 || target_ratio > 1.0) return RELAXKV_EINVAL;
+    double kt = floor(target_ratio * (double)p->T_c);           // floor(r_g T_c) in double
+    if (kt > (double)p->T_c) kt = (double)p->T_c;
+    return from_hip(launch_select_global(*p, scores, (int)kt, *s, g, targets, n_targets,
+                                         (hipStream_t)stream));
+}
+
+relaxkv_status relaxkv_build_sets_global(const relaxkv_problem* p, relaxkv_sets* s,
+                                         const int32_t* targets, const int32_t* n_targets,
+                                         void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!targets || !n_targets || !sets_match(p, s)) return RELAXKV_EINVAL;
+    st = from_hip(launch_build_sets_global(*p, *s, targets, n_targets, (hipStream_t)stream));
+    if (st == RELAXKV_OK) s->global_targets = 1;
+    return st;
 }
 
 relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets* s,

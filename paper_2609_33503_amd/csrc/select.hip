@@ -1,6 +1,10 @@
-// Per-layer top-k anchor selection (Sec. 3.2 / App. A.1: S_l = TopK_i(a_{l,i}, k)).
+// Per-layer top-k anchor selection (Sec. 3.2 / App. A.1: S_l = TopK_i(a_{l,i}, k)),
+// and the global target list of the target-capacity sweep (App. B equation:
+// g_i = (1/L) sum_l a_{l,i}, P = TopK_i(g_i, min(floor(r_g T_c), |U|))), which
+// runs the same selection on the single row g with the count capped on the
+// device by |U|.
 //
-// One 1024-thread workgroup per layer.  Scores are mapped to order-preserving
+// One 1024-thread workgroup per selected row.  Scores are mapped to order-preserving
 // unsigned keys (-0.0 folded onto +0.0), a 4 x 8-bit MSB-first radix select
 // finds the k-th largest key T and how many keys equal to T must be taken,
 // and a stable prefix-scan compaction in position order writes the anchors:
@@ -29,9 +33,15 @@ __global__ void clear_error_word(int32_t* counts, int L) {
     if (threadIdx.x == 0 && blockIdx.x == 0) counts[L + 1] = 0;
 }
 
+// Row blockIdx.x of `scores` [rows][T]: its k largest entries (k capped by
+// *k_cap when given), ascending positions into out + row * out_stride; the
+// count taken into *n_out when given.
 __global__ __launch_bounds__(kSelThreads) void select_topk(const float* __restrict__ scores,
                                                            int T, int k,
-                                                           int32_t* __restrict__ anchors,
+                                                           const int32_t* __restrict__ k_cap,
+                                                           int32_t* __restrict__ out_base,
+                                                           int out_stride,
+                                                           int32_t* __restrict__ n_out,
                                                            int32_t* __restrict__ counts, int L) {
     __shared__ int hist[256];
     __shared__ int scan_scratch[kSelThreads / 64];
@@ -39,6 +49,9 @@ __global__ __launch_bounds__(kSelThreads) void select_topk(const float* __restri
     const int l = blockIdx.x;
     const int tid = threadIdx.x;
     const float* a = scores + (size_t)l * T;
+    if (k_cap) k = min(k, k_cap[0]);
+    if (n_out && tid == 0) n_out[0] = max(k, 0);
+    if (k <= 0) return;                                  // nothing to select
 
     if (tid == 0) nan_sh = 0;
     int nan_seen = 0;
@@ -79,7 +92,7 @@ __global__ __launch_bounds__(kSelThreads) void select_topk(const float* __restri
     // prefix = the k-th largest key; k_rem = how many keys equal to it to take.
     const uint32_t thr = prefix;
     int eq_base = 0, sel_base = 0;
-    int32_t* out = anchors + (size_t)l * k;
+    int32_t* out = out_base + (size_t)l * out_stride;
     for (int base = 0; base < T; base += kSelThreads * kSelPerThread) {
         const int i0 = base + tid * kSelPerThread;
         uint32_t keys[kSelPerThread];
@@ -117,13 +130,33 @@ __global__ __launch_bounds__(kSelThreads) void select_topk(const float* __restri
     if (tid == 0 && nan_sh) atomicOr(&counts[L + 1], 1);
 }
 
+// g_i = (sum_l a_{l,i}) / L, the sum in layer order.
+__global__ void global_mean(const float* __restrict__ scores, int L, int T, float* __restrict__ g) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= T) return;
+    float acc = 0.f;
+    for (int l = 0; l < L; ++l) acc += scores[(size_t)l * T + i];
+    g[i] = acc / (float)L;
+}
+
 }  // namespace
 
 hipError_t launch_select(const relaxkv_problem& p, const float* scores, const relaxkv_sets& s,
                          hipStream_t st) {
     hipLaunchKernelGGL(clear_error_word, dim3(1), dim3(64), 0, st, s.counts, p.L);
     hipLaunchKernelGGL(select_topk, dim3(p.L), dim3(kSelThreads), 0, st, scores, p.T_c, s.k,
-                       s.anchors, s.counts, p.L);
+                       (const int32_t*)nullptr, s.anchors, s.k, (int32_t*)nullptr, s.counts, p.L);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_global(const relaxkv_problem& p, const float* scores, int k_target,
+                                const relaxkv_sets& s, float* g, int32_t* targets,
+                                int32_t* n_targets, hipStream_t st) {
+    hipLaunchKernelGGL(global_mean, dim3((p.T_c + 255) / 256), dim3(256), 0, st, scores, p.L,
+                       p.T_c, g);
+    // |P| = min(floor(r_g T_c), |U|) with |U| = counts[0] on the device.
+    hipLaunchKernelGGL(select_topk, dim3(1), dim3(kSelThreads), 0, st, (const float*)g, p.T_c,
+                       k_target, (const int32_t*)s.counts, targets, 0, n_targets, s.counts, p.L);
     return hipGetLastError();
 }
 

@@ -8,6 +8,12 @@
 // one workgroup that compacts U in position order and counts |R_l| from the
 // histogram of h; one workgroup per layer that compacts R_l out of U.  All
 // compactions are block prefix scans, so every output is deterministic.
+//
+// Matched-target variants (RelaxKV^G, Sec. 4.1 / App. A.3; the global target
+// sweep of App. B): U is built the same way from the anchors, then every layer
+// takes the same caller-given target list P.  A prefix maximum of the compact
+// map gives each target its compact limit |U cap {j <= p}| - 1 without any
+// search; targets need not lie in U.
 
 #include "dev_common.h"
 #include "internal.h"
@@ -167,9 +173,125 @@ __global__ __launch_bounds__(kSetThreads) void sets_layers(
     }
 }
 
-}  // namespace
+// ------------------------------------------------------ global target lists
 
-hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s, hipStream_t st) {
+__device__ __forceinline__ int wave_inclusive_max(int x) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x = max(x, y);
+    }
+    return x;
+}
+
+// Single workgroup.  last[i] = max_{j <= i} cidx[j] = |U cap {j <= i}| - 1
+// (written into h, which the last launch overwrites); checks the target list;
+// |R_l| = |P| and R_off for every layer.
+__global__ __launch_bounds__(kSetThreads) void gt_prefix(const int32_t* __restrict__ cidx, int T,
+                                                         int L, const int32_t* __restrict__ P,
+                                                         const int32_t* __restrict__ n_P,
+                                                         int32_t* __restrict__ last,
+                                                         int32_t* __restrict__ R_off,
+                                                         int32_t* __restrict__ counts) {
+    __shared__ int wmax[kSetThreads / 64];
+    __shared__ int bad_sh;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    if (tid == 0) bad_sh = 0;
+    int carry = -1;
+    for (int base = 0; base < T; base += kSetThreads * kSetPerThread) {
+        const int i0 = base + tid * kSetPerThread;
+        int v[kSetPerThread];
+        int m = -1;
+#pragma unroll
+        for (int e = 0; e < kSetPerThread; ++e) {
+            v[e] = i0 + e < T ? cidx[i0 + e] : -1;
+            m = max(m, v[e]);
+            v[e] = m;                                  // running max within the thread
+        }
+        const int incl = wave_inclusive_max(m);
+        if (lane == 63) wmax[w] = incl;
+        __syncthreads();
+        int before = carry;                            // max over earlier chunks and waves
+        for (int ww = 0; ww < w; ++ww) before = max(before, wmax[ww]);
+        int prev = __shfl_up(incl, 1, 64);             // earlier lanes of this wave
+        if (lane == 0) prev = -1;
+        const int excl = max(before, prev);
+        int blk = carry;
+        for (int ww = 0; ww < kSetThreads / 64; ++ww) blk = max(blk, wmax[ww]);
+#pragma unroll
+        for (int e = 0; e < kSetPerThread; ++e)
+            if (i0 + e < T) last[i0 + e] = max(excl, v[e]);
+        carry = blk;
+        __syncthreads();
+    }
+    // Target list checks: 0 <= |P| <= T, strictly ascending within [0, T).
+    const int n_raw = n_P[0];
+    const int n = min(max(n_raw, 0), T);
+    int bad = n_raw < 0 || n_raw > T;
+    for (int t = tid; t < n; t += kSetThreads) {
+        const int p = P[t];
+        bad |= p < 0 || p >= T || (t > 0 && P[t - 1] >= p);
+    }
+    if (bad) bad_sh = 1;                               // benign race: every writer stores 1
+    for (int l = tid; l <= L; l += kSetThreads) {
+        R_off[l] = l * n;
+        if (l < L) counts[1 + l] = n;
+    }
+    __syncthreads();
+    if (tid == 0 && bad_sh) atomicOr(&counts[L + 1], 2);
+}
+
+// One workgroup per layer: R_l = P, compact limits, the rank and source maps,
+// and the edge counts.
+__global__ __launch_bounds__(kSetThreads) void gt_layers(
+    const int32_t* __restrict__ last, const int32_t* __restrict__ U, int T,
+    const int32_t* __restrict__ P, const int32_t* __restrict__ R_off,
+    const int32_t* __restrict__ counts, int32_t* __restrict__ R_idx, int32_t* __restrict__ R_u,
+    int32_t* __restrict__ src, int32_t* __restrict__ rank, int64_t* __restrict__ edges, int L) {
+    __shared__ long long red[2][kSetThreads / 64];
+    const int l = blockIdx.x, tid = threadIdx.x;
+    const int nU = counts[0], n = counts[1 + l], off = R_off[l];
+    int32_t* src_l = src + (size_t)l * T;
+    int32_t* rank_l = rank + (size_t)l * T;
+    long long e_sum = 0, ef_sum = 0;
+    for (int t = tid; t < n; t += kSetThreads) {
+        const int p = min(max(P[t], 0), T - 1);        // in range even for a rejected list
+        const int u = last[p];
+        R_idx[off + t] = p;
+        R_u[off + t] = u;
+        rank_l[p] = t;
+        e_sum += u + 1;                                // |C_l(p)| = |U cap {j <= p}|
+        ef_sum += p + 1;
+    }
+    __syncthreads();                                   // rank_l complete for this layer
+    for (int c = tid; c < nU; c += kSetThreads) src_l[c] = rank_l[U[c]];
+    e_sum = wave_sum(e_sum);
+    ef_sum = wave_sum(ef_sum);
+    const int lane = tid & 63, w = tid >> 6;
+    if (lane == 0) {
+        red[0][w] = e_sum;
+        red[1][w] = ef_sum;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        long long a = 0, b = 0;
+        for (int i = 0; i < kSetThreads / 64; ++i) {
+            a += red[0][i];
+            b += red[1][i];
+        }
+        edges[l] = a;
+        edges[L + l] = b;
+    }
+}
+
+// h_i = L - 1 for targets, -1 otherwise (after gt_layers read the prefix maxima).
+__global__ void gt_h(const int32_t* __restrict__ rank0, int T, int L, int32_t* __restrict__ h) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < T; i += gridDim.x * blockDim.x)
+        h[i] = rank0[i] >= 0 ? L - 1 : -1;
+}
+
+void launch_union(const relaxkv_problem& p, const relaxkv_sets& s, hipStream_t st) {
     const int T = p.T_c, L = p.L;
     const long n_rank = (long)L * T;
     const long rb = (n_rank + 255) / 256;
@@ -181,6 +303,28 @@ hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s, hi
                        L, s.k, T, s.h);
     hipLaunchKernelGGL(sets_union, dim3(1), dim3(kSetThreads), 0, st, s.h, T, L, s.U, s.cidx,
                        s.R_off, s.counts);
+}
+
+}  // namespace
+
+hipError_t launch_build_sets_global(const relaxkv_problem& p, const relaxkv_sets& s,
+                                    const int32_t* targets, const int32_t* n_targets,
+                                    hipStream_t st) {
+    const int T = p.T_c, L = p.L;
+    launch_union(p, s, st);
+    hipLaunchKernelGGL(gt_prefix, dim3(1), dim3(kSetThreads), 0, st, s.cidx, T, L, targets,
+                       n_targets, s.h, s.R_off, s.counts);
+    hipLaunchKernelGGL(gt_layers, dim3(L), dim3(kSetThreads), 0, st, (const int32_t*)s.h, s.U, T,
+                       targets, s.R_off, s.counts, s.R_idx, s.R_u, s.src, s.rank, s.edges, L);
+    const int hb = (T + 255) / 256;
+    hipLaunchKernelGGL(gt_h, dim3(hb < 2048 ? hb : 2048), dim3(256), 0, st, (const int32_t*)s.rank,
+                       T, L, s.h);
+    return hipGetLastError();
+}
+
+hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s, hipStream_t st) {
+    const int T = p.T_c, L = p.L;
+    launch_union(p, s, st);
     hipLaunchKernelGGL(sets_layers, dim3(L), dim3(kSetThreads), 0, st, s.h, s.U, T, s.R_off,
                        s.counts, s.R_idx, s.R_u, s.src, s.rank, s.edges, L);
     return hipGetLastError();

@@ -23,8 +23,9 @@ CONTEXT_UNION, CONTEXT_FULL = 0, 1
 
 EXPORTS = ("relaxkv_status_string", "relaxkv_anchor_count", "relaxkv_validate",
            "relaxkv_score_workspace_bytes", "relaxkv_sets_bytes", "relaxkv_sets_bind",
-           "relaxkv_score", "relaxkv_select", "relaxkv_build_sets", "relaxkv_sparse_attn",
-           "relaxkv_update_cache", "relaxkv_counts_to_host")
+           "relaxkv_score", "relaxkv_select", "relaxkv_build_sets", "relaxkv_select_global",
+           "relaxkv_build_sets_global", "relaxkv_sparse_attn", "relaxkv_update_cache",
+           "relaxkv_counts_to_host")
 
 
 class RelaxKVError(RuntimeError):
@@ -46,7 +47,7 @@ class Sets(Structure):
                 ("anchors", c_void_p), ("h", c_void_p), ("U", c_void_p), ("cidx", c_void_p),
                 ("R_off", c_void_p), ("R_idx", c_void_p), ("R_u", c_void_p),
                 ("src", c_void_p), ("rank", c_void_p), ("counts", c_void_p),
-                ("edges", c_void_p)]
+                ("edges", c_void_p), ("global_targets", c_int32)]
 
 
 _lib = None
@@ -79,6 +80,12 @@ def load(path=None):
     lib.relaxkv_select.argtypes = [POINTER(Problem), c_void_p, POINTER(Sets), c_void_p]
     lib.relaxkv_build_sets.restype = c_int32
     lib.relaxkv_build_sets.argtypes = [POINTER(Problem), POINTER(Sets), c_void_p]
+    lib.relaxkv_select_global.restype = c_int32
+    lib.relaxkv_select_global.argtypes = [POINTER(Problem), c_void_p, c_double, POINTER(Sets),
+                                          c_void_p, c_void_p, c_void_p, c_void_p]
+    lib.relaxkv_build_sets_global.restype = c_int32
+    lib.relaxkv_build_sets_global.argtypes = [POINTER(Problem), POINTER(Sets), c_void_p, c_void_p,
+                                              c_void_p]
     lib.relaxkv_sparse_attn.restype = c_int32
     lib.relaxkv_sparse_attn.argtypes = [POINTER(Problem), POINTER(Sets), c_int32, c_void_p,
                                         c_void_p, c_void_p, c_void_p, c_void_p, c_int32,
@@ -188,6 +195,28 @@ class Request:
     def build_sets(self, sets, stream=None):
         _check(load().relaxkv_build_sets(ctypes.byref(self.p), ctypes.byref(sets.s),
                                          _stream(stream)), "relaxkv_build_sets")
+
+    # ---- matched-target variants: one global target list for every layer
+    def select_global(self, scores, target_ratio, sets, g, targets, n_targets, stream=None):
+        """g [T_c] f32, targets [T_c] int32 and n_targets [1] int32 are outputs."""
+        for t, dt, n in ((g, torch.float32, self.T_c), (targets, torch.int32, self.T_c),
+                         (n_targets, torch.int32, 1)):
+            if t.dtype != dt or not t.is_contiguous() or t.numel() < n:
+                raise ValueError("select_global outputs: g f32 [T_c], targets int32 [T_c], "
+                                 "n_targets int32 [1]")
+        _check(load().relaxkv_select_global(ctypes.byref(self.p), _ptr(scores),
+                                            float(target_ratio), ctypes.byref(sets.s), _ptr(g),
+                                            _ptr(targets), _ptr(n_targets), _stream(stream)),
+               "relaxkv_select_global")
+
+    def build_sets_global(self, sets, targets, n_targets, stream=None):
+        """targets: int32 device, ascending; n_targets: int32 device [1]."""
+        for t in (targets, n_targets):
+            if t.dtype != torch.int32 or not t.is_contiguous() or not t.is_cuda:
+                raise ValueError("targets and n_targets must be contiguous int32 device tensors")
+        _check(load().relaxkv_build_sets_global(ctypes.byref(self.p), ctypes.byref(sets.s),
+                                                _ptr(targets), _ptr(n_targets), _stream(stream)),
+               "relaxkv_build_sets_global")
 
     def sparse_attn(self, sets, layer, q_new, k_new, v_new, out, lse_out=None,
                     context_mode=CONTEXT_UNION, stream=None):

@@ -184,6 +184,22 @@ def test_compute_calls_reject_before_launch(rk):
                                     None) == rk.EINVAL
     assert lib.relaxkv_update_cache(ctypes.byref(other), ctypes.byref(s), 0, fake, fake, fake,
                                     fake, None) == rk.EINVAL
+    # select_global / build_sets_global (matched-target variants)
+    sg = lib.relaxkv_select_global
+    for r in (-0.1, 1.5, float("nan"), float("inf")):
+        assert sg(ctypes.byref(p), fake, r, ctypes.byref(s), fake, fake, fake, None) == rk.EINVAL
+    for i in range(4):
+        args_g = [fake, fake, fake, fake]
+        args_g[i] = None
+        scores_, g_, t_, n_ = args_g
+        assert sg(ctypes.byref(p), scores_, 0.2, ctypes.byref(s), g_, t_, n_, None) == rk.EINVAL
+    assert sg(ctypes.byref(other), fake, 0.2, ctypes.byref(s), fake, fake, fake, None) == rk.EINVAL
+    bg = lib.relaxkv_build_sets_global
+    assert bg(ctypes.byref(p), ctypes.byref(s), None, fake, None) == rk.EINVAL
+    assert bg(ctypes.byref(p), ctypes.byref(s), fake, None, None) == rk.EINVAL
+    assert bg(ctypes.byref(other), ctypes.byref(s), fake, fake, None) == rk.EINVAL
+    assert bg(ctypes.byref(p), None, fake, fake, None) == rk.EINVAL
+    assert s.global_targets == 0                     # unchanged by rejected calls
     # counts_to_host
     c = (ctypes.c_int32 * 6)()
     assert lib.relaxkv_counts_to_host(None, c, None, None) == rk.EINVAL
