@@ -298,6 +298,9 @@ def main():
     ap.add_argument("--control", action="store_true",
                     help="also time the Full-Prefix Control on the same targets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-matched-targets", action="store_true",
+                    help="skip the global-target sweep point (profiles of the main path's "
+                         "attention launches only)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run one plain device-to-device copy of MIB MiB (reference "
                          "kernel for scaling the HBM byte counters) and exit")
@@ -362,7 +365,8 @@ def main():
                      "avg_launch_ms": r["attn_launch_ms_avg"]},
     }
     res["cache_update"] = time_cache_update(b)
-    res["matched_targets"] = time_matched_targets(b)
+    if not args.no_matched_targets:
+        res["matched_targets"] = time_matched_targets(b)
     if args.control:
         rc = b.timed(args.steps, args.warmup, mode=relaxkv.CONTEXT_FULL)
         res["control"] = {"attn_ms_full_prefix": rc["attn_ms_total"],
