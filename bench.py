@@ -251,11 +251,16 @@ def cpu_baseline(b: Bench, budget_s=15.0):
         blas_threads = 1
     w = b.w
     l = 0
-    sets_ref_anchors = b.sets.anchors.cpu().numpy().astype(np.int64)
-    sets_ref = oracle.build_sets(sets_ref_anchors, w.T_c)
+    # The oracle's own schedule: its selection on seeded scores of the workload's
+    # shape (the union and active sets of iid scores match the workload's; no
+    # oracle input comes from the library), and layer 0's fresh rows for it.
+    a = np.random.default_rng(0).random((w.L, w.T_c))
+    sets_ref = oracle.build_sets(oracle.select(a, b.req.k), w.T_c)
     R_l = sets_ref.R[l]
     n = len(R_l)
-    fresh = tuple(synth.to_f64(t) for t in b.fresh[l])
+    qn, kn, vn = synth.make_fresh_layer(w, l, b.kc[l], b.vc[l], "cuda")
+    fresh = tuple(synth.to_f64(synth.gather_rows(t, R_l)) for t in (qn, kn, vn))
+    del qn, kn, vn
     kc, vc = synth.to_f64(b.kc[l]), synth.to_f64(b.vc[l])
     rng = np.random.default_rng(0)
     order = rng.permutation(n)

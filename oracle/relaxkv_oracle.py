@@ -25,6 +25,9 @@ with Sparse Context Attention for Efficient KV Cache Reuse"):
                       ``mode="full"``.
 * ``update_cache`` -- Sec. 3.4 cache-update semantics, Algorithm 1 update step:
                       fresh rows of R_l overwrite their cache positions.
+* ``build_sets_context`` -- the context-construction variants of Sec. 4.4
+                      (Global Sparse, Layerwise Sparse): the same anchors and
+                      targets with the context set U_l replaced.
 * ``global_scores``, ``global_target_count``, ``select_global``,
   ``build_sets_global`` -- the matched-target variants: RelaxKV^G (Sec. 4.1
                       comparison setup; App. A.3 table "Controlled
@@ -163,13 +166,19 @@ class Sets:
     cidx: np.ndarray                    # [T_c] compact index in U, -1 if not in U
     R: list = field(default_factory=list)       # R[l]: sorted positions
     R_u: list = field(default_factory=list)     # R_u[l][t]: compact index of R[l][t]
-    src: list = field(default_factory=list)     # src[l][c]: rank of U[c] in R[l] or -1
+    src: list = field(default_factory=list)     # src[l][c]: rank of context[l][c] in R[l] or -1
     edges: np.ndarray = None            # [L] sum_{p in R_l} |C_l(p)|
     edges_full: np.ndarray = None       # [L] sum_{p in R_l} (p + 1)
+    ctx: list = None                    # ctx[l]: sorted context set U_l; None: U at every layer
 
     @property
     def L(self):
         return len(self.R)
+
+    def context(self, layer):
+        """The context set U_l of a layer (the union U unless a construction
+        variant replaced it)."""
+        return self.U if self.ctx is None else self.ctx[layer]
 
 
 def build_sets(anchors, T_c):
@@ -219,6 +228,17 @@ def global_scores(a):
     """g_i = (1/L) sum_l a_{l,i}: the layer mean of the normalised scores (App. B)."""
     a = np.asarray(a, dtype=np.float64)
     return a.sum(axis=0) / a.shape[0]
+
+
+def global_scores_f32(a32):
+    """g in float32, the precision in which the GPU takes the TopK decision over
+    g: a float32 running sum over layers in layer order, then one float32
+    division by L (each step an IEEE-754 single operation)."""
+    a32 = np.asarray(a32, dtype=np.float32)
+    g = np.zeros(a32.shape[1], dtype=np.float32)
+    for l in range(a32.shape[0]):
+        g = (g + a32[l]).astype(np.float32)
+    return (g / np.float32(a32.shape[0])).astype(np.float32)
 
 
 def global_target_count(ratio, T_c, n_union):
@@ -281,6 +301,54 @@ def build_sets_global(anchors, T_c, P):
 
 
 # ----------------------------------------------------------------------------
+# Context-construction variants: Sec. 4.4 (Global Sparse, Layerwise Sparse).
+# ----------------------------------------------------------------------------
+
+def build_sets_context(anchors, T_c, a, construction, g=None):
+    """RelaxKV's anchors and targets R_l with the context set replaced by a
+    construction variant of the same size |U| (Sec. 4.4):
+
+    "union"      U_l = U, the union of the anchors (RelaxKV itself);
+    "global"     U_l = TopK_i(g_i, |U|) for every layer, g the layer mean of a
+                 (Global Sparse: one set shared across layers);
+    "layerwise"  U_l = TopK_i(a_{l,i}, |U|) (Layerwise Sparse).
+
+    g (optional) replaces the layer mean for "global", e.g. the float32 mean
+    in which a GPU ranks.  Ties go to the lower position.
+    C_l(p) = U_l cap {j <= p}: a target need not
+    lie in U_l (it then does not see its own key, and its context may be
+    empty).  R_u[l][t] = |U_l cap {j <= p}| - 1; src[l][c] = rank of U_l[c] in R_l
+    or -1; edges count |C_l(p)| over R_l; U, cidx and h stay those of the
+    anchor union.
+    """
+    base = build_sets(anchors, T_c)
+    a = np.asarray(a, dtype=np.float64)
+    L = len(base.R)
+    n = len(base.U)
+    if construction == "union":
+        ctx = [base.U.copy() for _ in range(L)]
+    elif construction == "global":
+        shared = select_global(global_scores(a) if g is None else g, n)
+        ctx = [shared.copy() for _ in range(L)]
+    elif construction == "layerwise":
+        ctx = [select(a[l:l + 1], n)[0] for l in range(L)]
+    else:
+        raise ValueError("construction must be 'union', 'global' or 'layerwise'")
+    R_u, src = [], []
+    edges = np.zeros(L, dtype=np.int64)
+    for l in range(L):
+        U_l = ctx[l]
+        n_le = np.array([int(np.count_nonzero(U_l <= p)) for p in base.R[l]], dtype=np.int64)
+        R_u.append(n_le - 1)
+        rank = np.full(T_c, -1, dtype=np.int64)
+        rank[base.R[l]] = np.arange(len(base.R[l]))
+        src.append(rank[U_l])
+        edges[l] = int(np.sum(n_le))
+    return Sets(T_c=T_c, k=base.k, anchors=base.anchors, h=base.h, U=base.U, cidx=base.cidx,
+                R=base.R, R_u=R_u, src=src, edges=edges, edges_full=base.edges_full, ctx=ctx)
+
+
+# ----------------------------------------------------------------------------
 # Sparse-context attention: Sec. 3.3, Sec. 3.4 equation, App. A.2.
 # ----------------------------------------------------------------------------
 
@@ -320,7 +388,7 @@ def sparse_attn(layer, sets, q_new, k_new, v_new, k_cache_l, v_cache_l,
     rank[R_l] = np.arange(n_R)
 
     if mode == "union":
-        ctx_all = sets.U
+        ctx_all = sets.context(layer)
     elif mode == "full":
         ctx_all = np.arange(sets.T_c)
     else:

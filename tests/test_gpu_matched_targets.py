@@ -97,20 +97,22 @@ def test_select_global_matches_oracle(gpu_lib, name):
     case = Case(SMALL[name])
     a, anchors = _anchors_and_sets(case, seed=41)
     case.req.build_sets(case.sets)
-    nU = case.sets.counts_to_host()[0][0]
+    nU = len(oracle.build_sets(anchors, case.T).U)
+    assert case.sets.counts_to_host()[0][0] == nU
     g = torch.empty(case.T, dtype=torch.float32, device="cuda")
     P = torch.empty(case.T, dtype=torch.int32, device="cuda")
     n = torch.empty(1, dtype=torch.int32, device="cuda")
     g_ref = oracle.global_scores(a.astype(np.float64))
+    g32 = oracle.global_scores_f32(a)                    # the ranking precision
     for r in (0.2, 0.5, 1.0, 1e-4):
         case.req.select_global(torch.from_numpy(a).cuda(), r, case.sets, g, P, n)
         torch.cuda.synchronize()
         g_gpu = g.cpu().numpy()
         np.testing.assert_allclose(g_gpu, g_ref, rtol=0, atol=4e-7 * case.L)
+        assert np.array_equal(g_gpu, g32)                # same fp32 operations in the same order
         n_ref = oracle.global_target_count(r, case.T, nU)
         assert int(n.item()) == n_ref
-        # integer outputs bit-exact when both sides rank the same fp32 g
-        P_ref = oracle.select_global(g_gpu.astype(np.float64), n_ref)
+        P_ref = oracle.select_global(g32.astype(np.float64), n_ref)
         assert P.cpu().numpy()[:n_ref].tolist() == P_ref.tolist()
 
 
@@ -192,17 +194,20 @@ def test_global_update_cache_bit_exact(gpu_lib, name):
 
 
 def test_full_size_global_target_sweep(gpu_lib):
-    """The 32K planted workload: scores from the GPU, anchors at r = 0.15,
-    P_{r_g} at r_g = 0.2 and the Target-Union cap (r_g = 1), sets bit-exact and
-    attention on sampled targets of sampled layers, as the benchmark runs it."""
+    """The 32K planted workload: seeded fp32 scores drive both sides, anchors at
+    r = 0.15, P_{r_g} at r_g = 0.2 and the Target-Union cap (r_g = 1), sets
+    bit-exact and attention on sampled targets of sampled layers, as the
+    benchmark runs it."""
     w = W["qwen14b-32k-planted"]
     case = Case(w)
-    a = case.gpu_scores()
-    anchors = case.gpu_select(a)
+    a_np = synthetic_scores(w.L, w.T_c, seed=49)
+    a = torch.from_numpy(a_np).cuda()
+    anchors = oracle.select(a_np.astype(np.float64), case.k)
+    assert np.array_equal(case.gpu_select(a), anchors)
     case.req.build_sets(case.sets)
-    nU = case.sets.counts_to_host()[0][0]
-    a_np = a.cpu().numpy()
-    assert np.array_equal(anchors, oracle.select(a_np.astype(np.float64), case.k))
+    nU = len(oracle.build_sets(anchors, case.T).U)
+    assert case.sets.counts_to_host()[0][0] == nU
+    g32 = oracle.global_scores_f32(a_np)
     g = torch.empty(case.T, dtype=torch.float32, device="cuda")
     P = torch.empty(case.T, dtype=torch.int32, device="cuda")
     n = torch.empty(1, dtype=torch.int32, device="cuda")
@@ -213,8 +218,9 @@ def test_full_size_global_target_sweep(gpu_lib):
         g_gpu = g.cpu().numpy()
         np.testing.assert_allclose(g_gpu, oracle.global_scores(a_np.astype(np.float64)),
                                    rtol=0, atol=4e-7 * case.L)
+        assert np.array_equal(g_gpu, g32)
         n_ref = oracle.global_target_count(r, case.T, nU)
-        P_ref = oracle.select_global(g_gpu.astype(np.float64), n_ref)
+        P_ref = oracle.select_global(g32.astype(np.float64), n_ref)
         assert int(n.item()) == n_ref
         assert P.cpu().numpy()[:n_ref].tolist() == P_ref.tolist()
         case.req.build_sets_global(case.sets, P, n)

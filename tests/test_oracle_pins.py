@@ -580,3 +580,107 @@ def test_attention_empty_context_is_empty_sum():
         x = kc[0, [4, 5]] @ qn[2, hh] / math.sqrt(d)
         w = np.exp(x - x.max())
         np.testing.assert_allclose(O[2, hh], (w / w.sum()) @ vc[0, [4, 5]], atol=1e-13)
+
+
+def test_global_scores_f32_rounding():
+    from oracle import global_scores, global_scores_f32
+    a = np.array([[0.5, 0.25, 1.0], [0.125, 0.75, 0.0], [0.375, 0.0, 0.5]], dtype=np.float32)
+    # sums of multiples of 1/8 are exact in fp32; only the division rounds
+    assert global_scores_f32(a).tolist() == np.float32([1.0 / 3, 1.0 / 3, 0.5]).tolist()
+    rng = np.random.default_rng(23)
+    a = rng.random((40, 500)).astype(np.float32)
+    g32 = global_scores_f32(a).astype(np.float64)
+    g64 = global_scores(a.astype(np.float64))
+    ulp = np.spacing(np.float32(1.0)).astype(np.float64)
+    assert np.max(np.abs(g32 - g64)) <= 40 * ulp                 # L roundings of values <= 1
+    assert global_scores_f32(a[:1]).tolist() == a[0].tolist()      # L = 1: the row itself
+
+
+# ----------------------------------------------------------------------------
+# context-construction variants (Global Sparse, Layerwise Sparse)
+# ----------------------------------------------------------------------------
+
+@settings(max_examples=50, deadline=None)
+@given(st.integers(1, 4), st.integers(1, 40), st.integers(0, 2**31 - 1), st.data(),
+       st.sampled_from(["union", "global", "layerwise"]))
+def test_build_sets_context_brute_force(L, T, seed, data, construction):
+    from oracle import build_sets_context
+    rng = np.random.default_rng(seed)
+    k = data.draw(st.integers(1, T))
+    a = rng.integers(0, 5, size=(L, T)) / 4.0                   # ties across positions
+    S = select(a, k)
+    base = build_sets(S, T)
+    s = build_sets_context(S, T, a, construction)
+    n = len(base.U)
+    for l in range(L):
+        if construction == "union":
+            want = base.U.tolist()
+        else:
+            sc = a.mean(axis=0) if construction == "global" else a[l]
+            want = sorted(sorted(range(T), key=lambda i: (-sc[i], i))[:n])
+        assert s.context(l).tolist() == want
+        assert len(want) == n                                     # same set size |U|
+        assert s.R[l].tolist() == base.R[l].tolist()              # targets unchanged
+        for t, p in enumerate(s.R[l].tolist()):
+            assert s.R_u[l][t] == sum(1 for j in want if j <= p) - 1
+        rank = {p: t for t, p in enumerate(s.R[l].tolist())}
+        assert s.src[l].tolist() == [rank.get(j, -1) for j in want]
+        assert s.edges[l] == sum(sum(1 for j in want if j <= p) for p in s.R[l].tolist())
+    assert s.edges_full.tolist() == base.edges_full.tolist()
+    assert s.U.tolist() == base.U.tolist() and s.h.tolist() == base.h.tolist()
+    if construction == "union":
+        for l in range(L):
+            assert s.R_u[l].tolist() == base.R_u[l].tolist()
+            assert s.src[l].tolist() == base.src[l].tolist()
+        assert s.edges.tolist() == base.edges.tolist()
+
+
+def test_context_global_equals_layerwise_for_identical_layers():
+    from oracle import build_sets_context
+    rng = np.random.default_rng(24)
+    L, T = 3, 60
+    a = np.tile(rng.random(T), (L, 1))
+    S = select(a, 7)
+    g, lw = build_sets_context(S, T, a, "global"), build_sets_context(S, T, a, "layerwise")
+    for l in range(L):
+        assert g.context(l).tolist() == lw.context(l).tolist()
+        assert g.R_u[l].tolist() == lw.R_u[l].tolist()
+
+
+@pytest.mark.parametrize("construction,mode", [("global", "union"), ("layerwise", "union"),
+                                               ("layerwise", "full")])
+def test_attention_context_variants_brute_force(construction, mode):
+    from oracle import build_sets_context
+    rng = np.random.default_rng(40)
+    L, T, H, H_kv, d = 3, 40, 4, 2, 8
+    a = rng.random((L, T))
+    S = select(a, 5)
+    s = build_sets_context(S, T, a, construction)
+    kc = rng.standard_normal((H_kv, T, d))
+    vc = rng.standard_normal((H_kv, T, d))
+    sigma = 1 / math.sqrt(d)
+    for l in range(L):
+        R = s.R[l].tolist()
+        n = len(R)
+        qn, kn, vn = (rng.standard_normal((n, hh, d)) for hh in (H, H_kv, H_kv))
+        O, lse = sparse_attn(l, s, qn, kn, vn, kc, vc, mode=mode)
+        ctx = set(s.context(l).tolist())
+        rank = {p: t for t, p in enumerate(R)}
+        for t, p in enumerate(R):
+            for hh in range(H):
+                g = hh // (H // H_kv)
+                terms = []
+                for j in range(T):
+                    if not ((j in ctx and j <= p) if mode == "union" else j <= p):
+                        continue
+                    kj = kn[rank[j], g] if j in rank else kc[g, j]
+                    vj = vn[rank[j], g] if j in rank else vc[g, j]
+                    terms.append((sigma * float(qn[t, hh] @ kj), vj))
+                if not terms:
+                    assert np.all(O[t, hh] == 0) and lse[t, hh] == -np.inf
+                    continue
+                m = max(x for x, _ in terms)
+                w = [math.exp(x - m) for x, _ in terms]
+                ref = sum(wi * vj for wi, (_, vj) in zip(w, terms)) / math.fsum(w)
+                np.testing.assert_allclose(O[t, hh], ref, atol=1e-12)
+                assert lse[t, hh] == pytest.approx(m + math.log(math.fsum(w)), abs=1e-12)
