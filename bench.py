@@ -213,6 +213,42 @@ def time_matched_targets(b: Bench, target_ratio=0.2, reps=2):
             "edges": E, "edges_full_prefix": float(sum(edges[w.L:]))}
 
 
+def time_context_variants(b: Bench, reps=2):
+    """Context-construction variants (Sec. 4.4) on the same anchors and targets:
+    Global Sparse (top-|U| of the layer-mean score for every layer) and
+    Layerwise Sparse (top-|U| per layer).  Times relaxkv_build_sets_context and
+    the 40 attention launches over the same fresh rows; the RelaxKV sets are
+    rebuilt afterwards."""
+    w = b.w
+    req, sets = b.req, b.sets
+    mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    res = {}
+    for name, c in (("global_sparse", relaxkv.CONTEXT_SETS_GLOBAL),
+                    ("layerwise_sparse", relaxkv.CONTEXT_SETS_LAYERWISE)):
+        ms_sets, ms_attn = [], []
+        for i in range(reps + 1):
+            e0, e1, e2 = mk(), mk(), mk()
+            e0.record()
+            req.build_sets_context(b.scores, c, sets)
+            e1.record()
+            for l in range(w.L):
+                req.sparse_attn(sets, l, *b.fresh[l], b.out[l], None)
+            e2.record()
+            torch.cuda.synchronize()
+            if i:
+                ms_sets.append(e0.elapsed_time(e1))
+                ms_attn.append(e1.elapsed_time(e2))
+        counts, edges = sets.counts_to_host()
+        E = float(sum(edges[:w.L]))
+        attn_ms = float(np.mean(ms_attn))
+        res[name] = {"context_size": counts[0], "build_sets_ms": float(np.mean(ms_sets)),
+                     "attn_ms_all_layers": attn_ms,
+                     "attn_tflops": 4.0 * w.H * w.d * E / (attn_ms * 1e-3) / 1e12, "edges": E}
+    req.build_sets(sets)                     # back to RelaxKV's union context
+    torch.cuda.synchronize()
+    return res
+
+
 def time_scoring_supplied_lse(b: Bench, reps=5):
     """Time relaxkv_score in its one-pass mode: each query row's log-sum-exp is
     supplied, as the query's own forward pass would produce it (computed here
@@ -304,8 +340,8 @@ def main():
                     help="also time the Full-Prefix Control on the same targets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-matched-targets", action="store_true",
-                    help="skip the global-target sweep point (profiles of the main path's "
-                         "attention launches only)")
+                    help="skip the global-target sweep point and the context-construction "
+                         "variants (profiles of the main path's attention launches only)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run one plain device-to-device copy of MIB MiB (reference "
                          "kernel for scaling the HBM byte counters) and exit")
@@ -372,6 +408,7 @@ def main():
     res["cache_update"] = time_cache_update(b)
     if not args.no_matched_targets:
         res["matched_targets"] = time_matched_targets(b)
+        res["context_variants"] = time_context_variants(b)
     if args.control:
         rc = b.timed(args.steps, args.warmup, mode=relaxkv.CONTEXT_FULL)
         res["control"] = {"attn_ms_full_prefix": rc["attn_ms_total"],

@@ -15,8 +15,10 @@
  *                       with the mixed fresh/cached K~, V~ rule          (Sec. 3.3, 3.4, App. A.2)
  *
  * plus the cache update of the repaired rows (relaxkv_update_cache, Sec. 3.4)
- * and the matched-target variants, where one global target list replaces R_l
- * (relaxkv_select_global, relaxkv_build_sets_global; Sec. 4.1, App. A.3, App. B).
+ * the matched-target variants, where one global target list replaces R_l
+ * (relaxkv_select_global, relaxkv_build_sets_global; Sec. 4.1, App. A.3, App. B),
+ * and the context-construction variants, where another context set of the same
+ * size replaces U (relaxkv_build_sets_context; Sec. 4.4).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -57,8 +59,13 @@ typedef int32_t relaxkv_status;
 #define RELAXKV_DTYPE_F32  0
 #define RELAXKV_DTYPE_BF16 1
 
-#define RELAXKV_CONTEXT_UNION 0  /* C_l(p) = U cap {j <= p} (RelaxKV, Sec. 3.3) */
+#define RELAXKV_CONTEXT_UNION 0  /* C_l(p) = U_l cap {j <= p} (RelaxKV, Sec. 3.3) */
 #define RELAXKV_CONTEXT_FULL  1  /* {j <= p}: Full-Prefix Control (App. A.3) */
+
+/* Context set U_l of relaxkv_build_sets_context (Sec. 4.4). */
+#define RELAXKV_CONTEXT_SETS_UNION     0  /* U_l = U, the anchor union (RelaxKV) */
+#define RELAXKV_CONTEXT_SETS_GLOBAL    1  /* U_l = TopK(g, |U|) for every layer (Global Sparse) */
+#define RELAXKV_CONTEXT_SETS_LAYERWISE 2  /* U_l = TopK(a_l, |U|) per layer (Layerwise Sparse) */
 
 /* Limits of this build (checked by relaxkv_validate). */
 #define RELAXKV_MAX_LAYERS 1024
@@ -101,9 +108,12 @@ typedef struct relaxkv_problem {
  *   cidx     [T_c]         compact index of position i in U, -1 if i not in U.
  *   R_off    [L+1]         R_l occupies entries R_off[l] .. R_off[l+1]-1 of R_idx/R_u.
  *   R_idx    [L*T_c]       positions of R_l, ascending (CSR over layers).
- *   R_u      [L*T_c]       compact index (in U) of each R_idx entry.
- *   src      [L][T_c]      src[l*T_c + c] = rank of U[c] within R_l (its row in the
- *                          fresh K/V of layer l), or -1 (cached row), c < |U|.
+ *   R_u      [L*T_c]       compact limit of each R_idx entry: |U_l cap {j <= p}| - 1
+ *                          (its compact index when p is in U_l; -1 for an empty context).
+ *   src      [L][T_c]      src[l*T_c + c] = rank of U_l[c] within R_l (its row in the
+ *                          fresh K/V of layer l), or -1 (cached row), c < |U|; U_l is
+ *                          the layer's context list (U unless a construction variant
+ *                          replaced it, see ctx).
  *   rank     [L][T_c]      rank[l*T_c + j] = rank of position j within R_l, or -1 when j is
  *                          not an active target of layer l (position-indexed view of src).
  *   counts   [L+2]         counts[0] = |U|; counts[1+l] = |R_l|; counts[L+1] = error
@@ -112,12 +122,20 @@ typedef struct relaxkv_problem {
  *                          got an invalid target list (cleared by relaxkv_select).
  *   edges    [2L]          edges[l] = sum_{p in R_l} |C_l(p)| (App. A.2 edge count);
  *                          edges[L+l] = sum_{p in R_l} (p+1), the full-prefix count.
+ *   ctx      [L][T_c]      context lists of the construction variants (first |U| entries
+ *                          of a row, ascending): row 0 for every layer (Global Sparse) or
+ *                          row l for layer l (Layerwise Sparse); unused for the union.
+ *   g        [T_c]         float32 layer-mean scores of the last Global Sparse build.
  *   k        the anchor budget k = max(1, round(r T_c)), computed on the host.
  *   global_targets  host flag: 0 after relaxkv_sets_bind and relaxkv_build_sets
  *                   (targets R_l of RelaxKV, |R_l| <= min(T_c, (L-l) k)), 1 after
  *                   relaxkv_build_sets_global (one target list for every layer,
  *                   |R_l| <= T_c); the attention and cache-update calls size their
  *                   grids from it.
+ *   context_sets    host flag: the RELAXKV_CONTEXT_SETS_* construction of U_l of the
+ *                   last set build (0 after relaxkv_sets_bind, relaxkv_build_sets and
+ *                   relaxkv_build_sets_global); relaxkv_sparse_attn reads U_l from
+ *                   U or ctx accordingly.
  */
 typedef struct relaxkv_sets {
     int32_t L, T_c, k;
@@ -132,7 +150,10 @@ typedef struct relaxkv_sets {
     int32_t* rank;
     int32_t* counts;
     int64_t* edges;
+    int32_t* ctx;
+    float* g;
     int32_t global_targets;
+    int32_t context_sets;
 } relaxkv_sets;
 
 /* Text of a status code (static storage). */
@@ -194,6 +215,27 @@ relaxkv_status relaxkv_select(const relaxkv_problem* p, const float* scores,
  * s->global_targets = 0.
  */
 relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, relaxkv_sets* s, void* stream);
+
+/*
+ * Context-construction variants (Sec. 4.4): RelaxKV's anchors S_l (s->anchors)
+ * and active targets R_l, with the context set U_l replaced by one of the same
+ * size |U| (the anchor union's size):
+ *   RELAXKV_CONTEXT_SETS_UNION      U_l = U (the same sets as relaxkv_build_sets);
+ *   RELAXKV_CONTEXT_SETS_GLOBAL     U_l = TopK_i(g_i, |U|) for every layer, with
+ *                                   g_i = (1/L) sum_l a_{l,i} (Global Sparse);
+ *   RELAXKV_CONTEXT_SETS_LAYERWISE  U_l = TopK_i(a_{l,i}, |U|) (Layerwise Sparse);
+ * larger scores first, equal scores to the lower position.  C_l(p) = U_l cap
+ * {j <= p}; K~/V~ are fresh for j in R_l.  A target need not lie in U_l (it then
+ * does not see its own key; an empty context gives O = 0, lse = -inf).  h, U,
+ * cidx, R_idx and the full-prefix edge counts are those of relaxkv_build_sets;
+ * R_u, src and edges[0..L-1] refer to U_l; the lists go to s->ctx and g to s->g.
+ *   scores        device [L][T_c] float32 (a_{l,i}); a NaN sets bit 0 of the error word.
+ *   construction  one of RELAXKV_CONTEXT_SETS_*.
+ * Sets s->context_sets = construction and s->global_targets = 0.
+ */
+relaxkv_status relaxkv_build_sets_context(const relaxkv_problem* p, const float* scores,
+                                          int32_t construction, relaxkv_sets* s,
+                                          void* stream);
 
 /*
  * Global repair targets of the target-capacity sweep (App. B equation):

@@ -476,7 +476,10 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.v_new = v_new;
     a.kc = (const char*)p.k_cache + (size_t)layer * layer_elems * esz;
     a.vc = (const char*)p.v_cache + (size_t)layer * layer_elems * esz;
-    a.U = s.U;
+    // The layer's context list: the union, or a construction variant's list.
+    a.U = s.context_sets == RELAXKV_CONTEXT_SETS_GLOBAL      ? s.ctx
+          : s.context_sets == RELAXKV_CONTEXT_SETS_LAYERWISE ? s.ctx + (size_t)layer * p.T_c
+                                                             : s.U;
     a.cidx = s.cidx;
     a.src_l = s.src + (size_t)layer * p.T_c;
     a.rank_l = s.rank + (size_t)layer * p.T_c;

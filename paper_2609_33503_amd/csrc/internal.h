@@ -32,6 +32,12 @@ hipError_t launch_select(const relaxkv_problem& p, const float* scores,
 hipError_t launch_select_global(const relaxkv_problem& p, const float* scores, int k_target,
                                 const relaxkv_sets& s, float* g, int32_t* targets,
                                 int32_t* n_targets, hipStream_t st);
+hipError_t launch_build_sets_context(const relaxkv_problem& p, const float* scores,
+                                     int construction, const relaxkv_sets& s, hipStream_t st);
+hipError_t launch_select_rows(const float* scores, int n_rows, int T, int k, const int32_t* k_cap,
+                              int32_t* out, int out_stride, int32_t* counts, int L,
+                              hipStream_t st);
+hipError_t launch_global_mean(const float* scores, int L, int T, float* g, hipStream_t st);
 hipError_t launch_build_sets_global(const relaxkv_problem& p, const relaxkv_sets& s,
                                     const int32_t* targets, const int32_t* n_targets,
                                     hipStream_t st);

@@ -24,7 +24,7 @@ bool dims_ok(const relaxkv_problem* p) {
 
 // Byte sizes of the set arrays, in carving order.
 struct SetsLayout {
-    size_t anchors, h, U, cidx, R_off, R_idx, R_u, src, rank, counts, edges, total;
+    size_t anchors, h, U, cidx, R_off, R_idx, R_u, src, rank, counts, edges, ctx, g, total;
 };
 
 SetsLayout sets_layout(const relaxkv_problem* p, int32_t k) {
@@ -41,8 +41,10 @@ SetsLayout sets_layout(const relaxkv_problem* p, int32_t k) {
     s.rank = align_up(L * T * 4);
     s.counts = align_up((L + 2) * 4);
     s.edges = align_up(2 * L * 8);
+    s.ctx = align_up(L * T * 4);
+    s.g = align_up(T * 4);
     s.total = s.anchors + s.h + s.U + s.cidx + s.R_off + s.R_idx + s.R_u + s.src + s.rank + s.counts +
-              s.edges;
+              s.edges + s.ctx + s.g;
     return s;
 }
 
@@ -50,7 +52,9 @@ bool sets_match(const relaxkv_problem* p, const relaxkv_sets* s) {
     return s && s->L == p->L && s->T_c == p->T_c &&
            s->k == relaxkv_anchor_count(p->anchor_ratio, p->T_c) && s->anchors && s->h &&
            s->U && s->cidx && s->R_off && s->R_idx && s->R_u && s->src && s->rank && s->counts &&
-           s->edges;
+           s->edges && s->ctx && s->g &&
+           s->context_sets >= RELAXKV_CONTEXT_SETS_UNION &&
+           s->context_sets <= RELAXKV_CONTEXT_SETS_LAYERWISE;
 }
 
 relaxkv_status from_hip(hipError_t e) { return e == hipSuccess ? RELAXKV_OK : RELAXKV_EDEVICE; }
@@ -127,8 +131,11 @@ relaxkv_status relaxkv_sets_bind(const relaxkv_problem* p, void* dev_buf, size_t
     s.src = (int32_t*)b; b += l.src;
     s.rank = (int32_t*)b; b += l.rank;
     s.counts = (int32_t*)b; b += l.counts;
-    s.edges = (int64_t*)b;
+    s.edges = (int64_t*)b; b += l.edges;
+    s.ctx = (int32_t*)b; b += l.ctx;
+    s.g = (float*)b;
     s.global_targets = 0;
+    s.context_sets = RELAXKV_CONTEXT_SETS_UNION;
     *out = s;
     return RELAXKV_OK;
 }
@@ -156,7 +163,25 @@ relaxkv_status relaxkv_build_sets(const relaxkv_problem* p, relaxkv_sets* s, voi
     if (st != RELAXKV_OK) return st;
     if (!sets_match(p, s)) return RELAXKV_EINVAL;
     st = from_hip(launch_build_sets(*p, *s, (hipStream_t)stream));
-    if (st == RELAXKV_OK) s->global_targets = 0;
+    if (st == RELAXKV_OK) {
+        s->global_targets = 0;
+        s->context_sets = RELAXKV_CONTEXT_SETS_UNION;
+    }
+    return st;
+}
+
+relaxkv_status relaxkv_build_sets_context(const relaxkv_problem* p, const float* scores,
+                                          int32_t construction, relaxkv_sets* s, void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (!scores || !sets_match(p, s)) return RELAXKV_EINVAL;
+    if (construction < RELAXKV_CONTEXT_SETS_UNION || construction > RELAXKV_CONTEXT_SETS_LAYERWISE)
+        return RELAXKV_EINVAL;
+    st = from_hip(launch_build_sets_context(*p, scores, construction, *s, (hipStream_t)stream));
+    if (st == RELAXKV_OK) {
+        s->global_targets = 0;
+        s->context_sets = construction;
+    }
     return st;
 }
 
@@ -180,7 +205,10 @@ relaxkv_status relaxkv_build_sets_global(const relaxkv_problem* p, relaxkv_sets*
     if (st != RELAXKV_OK) return st;
     if (!targets || !n_targets || !sets_match(p, s)) return RELAXKV_EINVAL;
     st = from_hip(launch_build_sets_global(*p, *s, targets, n_targets, (hipStream_t)stream));
-    if (st == RELAXKV_OK) s->global_targets = 1;
+    if (st == RELAXKV_OK) {
+        s->global_targets = 1;
+        s->context_sets = RELAXKV_CONTEXT_SETS_UNION;
+    }
     return st;
 }
 

@@ -149,6 +149,19 @@ hipError_t launch_select(const relaxkv_problem& p, const float* scores, const re
     return hipGetLastError();
 }
 
+hipError_t launch_select_rows(const float* scores, int n_rows, int T, int k, const int32_t* k_cap,
+                              int32_t* out, int out_stride, int32_t* counts, int L,
+                              hipStream_t st) {
+    hipLaunchKernelGGL(select_topk, dim3(n_rows), dim3(kSelThreads), 0, st, scores, T, k, k_cap,
+                       out, out_stride, (int32_t*)nullptr, counts, L);
+    return hipGetLastError();
+}
+
+hipError_t launch_global_mean(const float* scores, int L, int T, float* g, hipStream_t st) {
+    hipLaunchKernelGGL(global_mean, dim3((T + 255) / 256), dim3(256), 0, st, scores, L, T, g);
+    return hipGetLastError();
+}
+
 hipError_t launch_select_global(const relaxkv_problem& p, const float* scores, int k_target,
                                 const relaxkv_sets& s, float* g, int32_t* targets,
                                 int32_t* n_targets, hipStream_t st) {

@@ -14,6 +14,11 @@
 // takes the same caller-given target list P.  A prefix maximum of the compact
 // map gives each target its compact limit |U cap {j <= p}| - 1 without any
 // search; targets need not lie in U.
+//
+// Context-construction variants (Sec. 4.4): the same anchors and targets R_l;
+// the context list of a layer is replaced by a top-|U| list (of the layer-mean
+// score, shared, or of the layer's score), written to ctx; the compact limits,
+// source map and edge counts are recomputed against it.
 
 #include "dev_common.h"
 #include "internal.h"
@@ -291,6 +296,46 @@ __global__ void gt_h(const int32_t* __restrict__ rank0, int T, int L, int32_t* _
         h[i] = rank0[i] >= 0 ? L - 1 : -1;
 }
 
+// ------------------------------------------------ context-construction variants
+
+// One workgroup per layer: compact limits of RelaxKV's targets R_l within the
+// layer's context list U_l (upper bound by binary search: both are ascending),
+// the source map over U_l and the edge counts.
+__global__ __launch_bounds__(kSetThreads) void ctx_layers(
+    const int32_t* __restrict__ ctx, int ctx_stride, int T, const int32_t* __restrict__ R_off,
+    const int32_t* __restrict__ R_idx, const int32_t* __restrict__ counts,
+    const int32_t* __restrict__ rank, int32_t* __restrict__ R_u, int32_t* __restrict__ src,
+    int64_t* __restrict__ edges, int L) {
+    __shared__ long long red[kSetThreads / 64];
+    const int l = blockIdx.x, tid = threadIdx.x;
+    const int32_t* ctx_l = ctx + (size_t)l * ctx_stride;
+    const int n = counts[0];                           // every context list has |U| entries
+    const int off = R_off[l], nR = counts[1 + l];
+    const int32_t* rank_l = rank + (size_t)l * T;
+    int32_t* src_l = src + (size_t)l * T;
+    long long e_sum = 0;
+    for (int t = tid; t < nR; t += kSetThreads) {
+        const int p = R_idx[off + t];
+        int lo = 0, hi = n;                            // first entry > p
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (ctx_l[mid] <= p) lo = mid + 1;
+            else hi = mid;
+        }
+        R_u[off + t] = lo - 1;
+        e_sum += lo;                                   // |U_l cap {j <= p}|
+    }
+    for (int c = tid; c < n; c += kSetThreads) src_l[c] = rank_l[ctx_l[c]];
+    e_sum = wave_sum(e_sum);
+    if ((tid & 63) == 0) red[tid >> 6] = e_sum;
+    __syncthreads();
+    if (tid == 0) {
+        long long a = 0;
+        for (int i = 0; i < kSetThreads / 64; ++i) a += red[i];
+        edges[l] = a;
+    }
+}
+
 void launch_union(const relaxkv_problem& p, const relaxkv_sets& s, hipStream_t st) {
     const int T = p.T_c, L = p.L;
     const long n_rank = (long)L * T;
@@ -306,6 +351,25 @@ void launch_union(const relaxkv_problem& p, const relaxkv_sets& s, hipStream_t s
 }
 
 }  // namespace
+
+hipError_t launch_build_sets_context(const relaxkv_problem& p, const float* scores,
+                                     int construction, const relaxkv_sets& s, hipStream_t st) {
+    const int T = p.T_c, L = p.L;
+    hipError_t e = launch_build_sets(p, s, st);       // anchors -> h, U, R_l, rank (+ union maps)
+    if (e != hipSuccess || construction == RELAXKV_CONTEXT_SETS_UNION) return e;
+    // Top-|U| context lists, ascending (the k cap |U| is read on the device).
+    if (construction == RELAXKV_CONTEXT_SETS_GLOBAL) {
+        e = launch_global_mean(scores, L, T, s.g, st);
+        if (e == hipSuccess) e = launch_select_rows(s.g, 1, T, T, s.counts, s.ctx, 0, s.counts, L, st);
+    } else {
+        e = launch_select_rows(scores, L, T, T, s.counts, s.ctx, T, s.counts, L, st);
+    }
+    if (e != hipSuccess) return e;
+    const int stride = construction == RELAXKV_CONTEXT_SETS_GLOBAL ? 0 : T;
+    hipLaunchKernelGGL(ctx_layers, dim3(L), dim3(kSetThreads), 0, st, (const int32_t*)s.ctx, stride,
+                       T, s.R_off, s.R_idx, s.counts, s.rank, s.R_u, s.src, s.edges, L);
+    return hipGetLastError();
+}
 
 hipError_t launch_build_sets_global(const relaxkv_problem& p, const relaxkv_sets& s,
                                     const int32_t* targets, const int32_t* n_targets,

@@ -20,10 +20,12 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librelaxkv
 OK, EINVAL, ENOSPACE, EUNSUPPORTED, EDEVICE = 0, -1, -2, -3, -4
 DTYPE_F32, DTYPE_BF16 = 0, 1
 CONTEXT_UNION, CONTEXT_FULL = 0, 1
+CONTEXT_SETS_UNION, CONTEXT_SETS_GLOBAL, CONTEXT_SETS_LAYERWISE = 0, 1, 2
 
 EXPORTS = ("relaxkv_status_string", "relaxkv_anchor_count", "relaxkv_validate",
            "relaxkv_score_workspace_bytes", "relaxkv_sets_bytes", "relaxkv_sets_bind",
-           "relaxkv_score", "relaxkv_select", "relaxkv_build_sets", "relaxkv_select_global",
+           "relaxkv_score", "relaxkv_select", "relaxkv_build_sets", "relaxkv_build_sets_context",
+           "relaxkv_select_global",
            "relaxkv_build_sets_global", "relaxkv_sparse_attn", "relaxkv_update_cache",
            "relaxkv_counts_to_host")
 
@@ -47,7 +49,8 @@ class Sets(Structure):
                 ("anchors", c_void_p), ("h", c_void_p), ("U", c_void_p), ("cidx", c_void_p),
                 ("R_off", c_void_p), ("R_idx", c_void_p), ("R_u", c_void_p),
                 ("src", c_void_p), ("rank", c_void_p), ("counts", c_void_p),
-                ("edges", c_void_p), ("global_targets", c_int32)]
+                ("edges", c_void_p), ("ctx", c_void_p), ("g", c_void_p),
+                ("global_targets", c_int32), ("context_sets", c_int32)]
 
 
 _lib = None
@@ -80,6 +83,9 @@ def load(path=None):
     lib.relaxkv_select.argtypes = [POINTER(Problem), c_void_p, POINTER(Sets), c_void_p]
     lib.relaxkv_build_sets.restype = c_int32
     lib.relaxkv_build_sets.argtypes = [POINTER(Problem), POINTER(Sets), c_void_p]
+    lib.relaxkv_build_sets_context.restype = c_int32
+    lib.relaxkv_build_sets_context.argtypes = [POINTER(Problem), c_void_p, c_int32, POINTER(Sets),
+                                               c_void_p]
     lib.relaxkv_select_global.restype = c_int32
     lib.relaxkv_select_global.argtypes = [POINTER(Problem), c_void_p, c_double, POINTER(Sets),
                                           c_void_p, c_void_p, c_void_p, c_void_p]
@@ -196,6 +202,13 @@ class Request:
         _check(load().relaxkv_build_sets(ctypes.byref(self.p), ctypes.byref(sets.s),
                                          _stream(stream)), "relaxkv_build_sets")
 
+    def build_sets_context(self, scores, construction, sets, stream=None):
+        """RelaxKV's anchors and targets with the context set replaced
+        (CONTEXT_SETS_UNION / _GLOBAL / _LAYERWISE); scores [L][T_c] f32."""
+        _check(load().relaxkv_build_sets_context(ctypes.byref(self.p), _ptr(scores),
+                                                 int(construction), ctypes.byref(sets.s),
+                                                 _stream(stream)), "relaxkv_build_sets_context")
+
     # ---- matched-target variants: one global target list for every layer
     def select_global(self, scores, target_ratio, sets, g, targets, n_targets, stream=None):
         """g [T_c] f32, targets [T_c] int32 and n_targets [1] int32 are outputs."""
@@ -267,6 +280,8 @@ class SetsBuffer:
         self.rank = view(s.rank, L * T, torch.int32).view(L, T)
         self.counts = view(s.counts, L + 2, torch.int32)
         self.edges = view(s.edges, 2 * L, torch.int64)
+        self.ctx = view(s.ctx, L * T, torch.int32).view(L, T)
+        self.g = view(s.g, T, torch.float32)
 
     def counts_to_host(self, stream=None):
         """(counts [L+2], edges [2L]) on the host; synchronises the stream."""

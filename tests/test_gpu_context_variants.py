@@ -1,0 +1,133 @@
+"""GPU parity of the context-construction variants (Sec. 4.4) against the
+float64 oracle: RelaxKV's anchors and targets with the context set replaced by
+the top-|U| positions of the layer-mean score (Global Sparse) or of each
+layer's score (Layerwise Sparse).  Set arrays bit-exact on shared fp32 scores
+(g compared bit-exactly with the oracle's float32 layer mean, the precision the
+ranking uses); attention within 2e-2 max-abs (bf16) / 1e-5 relative (fp32);
+empty contexts give O = 0 and lse = -inf.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from harness import Case, assert_close, synthetic_scores
+from paper_2609_33503_amd import relaxkv, synth
+
+pytestmark = pytest.mark.gpu
+
+W = synth.WORKLOADS
+SMALL = {
+    "tiny": W["tiny-2L-1k-fp32"],
+    "qwen-planted": synth.shrink(W["qwen14b-32k-planted"], L=4, T_c=2600),
+    "d64-bf16": synth.shrink(W["llama8b-8k"], L=2, T_c=777, H=8, H_kv=2, d=64, Qn=24),
+}
+CONS = {"union": relaxkv.CONTEXT_SETS_UNION, "global": relaxkv.CONTEXT_SETS_GLOBAL,
+        "layerwise": relaxkv.CONTEXT_SETS_LAYERWISE}
+
+
+def build_both(case, a32, construction):
+    """GPU sets from the fp32 scores a32 and the oracle's from the same values."""
+    anchors = oracle.select(a32.astype(np.float64), case.k)
+    a_dev = torch.from_numpy(a32).cuda()
+    case.req.select(a_dev, case.sets)
+    case.req.build_sets_context(a_dev, CONS[construction], case.sets)
+    ref = oracle.build_sets_context(anchors, case.T, a32.astype(np.float64), construction,
+                                    g=oracle.global_scores_f32(a32).astype(np.float64))
+    return anchors, ref
+
+
+def compare_context_sets(case, ref, construction):
+    counts, edges = case.sets.counts_to_host()
+    L, T = case.L, case.T
+    n = counts[0]
+    assert n == len(ref.U)
+    assert case.sets.anchors.cpu().numpy().tolist() == ref.anchors.tolist()
+    assert case.sets.h.cpu().numpy().tolist() == ref.h.tolist()
+    assert case.sets.U.cpu().numpy()[:n].tolist() == ref.U.tolist()
+    R_off = case.sets.R_off.cpu().numpy()
+    R_idx = case.sets.R_idx.cpu().numpy()
+    R_u = case.sets.R_u.cpu().numpy()
+    src = case.sets.src.cpu().numpy()
+    ctx = case.sets.ctx.cpu().numpy()
+    for l in range(L):
+        assert counts[1 + l] == len(ref.R[l])
+        assert R_idx[R_off[l]:R_off[l + 1]].tolist() == ref.R[l].tolist()
+        assert R_u[R_off[l]:R_off[l + 1]].tolist() == ref.R_u[l].tolist()
+        assert src[l, :n].tolist() == ref.src[l].tolist()
+        if construction == "global":
+            assert ctx[0, :n].tolist() == ref.context(l).tolist()
+        elif construction == "layerwise":
+            assert ctx[l, :n].tolist() == ref.context(l).tolist()
+        assert edges[l] == int(ref.edges[l])
+        assert edges[L + l] == int(ref.edges_full[l])
+    assert counts[L + 1] == 0
+    assert case.sets.s.context_sets == CONS[construction]
+
+
+def _compare_attn(case, out, lse, O_ref, lse_ref, what):
+    empty = np.isneginf(lse_ref[:, 0])
+    got_O = out.float().cpu().numpy()
+    got_lse = lse.cpu().numpy()
+    assert np.all(got_O[empty] == 0.0) and np.all(np.isneginf(got_lse[empty])), what
+    if (~empty).any():
+        assert_close(got_O[~empty], O_ref[~empty], case.w, what,
+                     rel_gate=1e-2 if case.w.dtype == "bf16" else None)
+        assert_close(got_lse[~empty], lse_ref[~empty], case.w, what + " lse")
+
+
+@pytest.mark.parametrize("construction", ["global", "layerwise", "union"])
+@pytest.mark.parametrize("name", list(SMALL))
+def test_context_variant_sets_and_attention(gpu_lib, name, construction):
+    case = Case(SMALL[name])
+    a_ref, _, _ = case.oracle_scores()
+    a32 = a_ref.astype(np.float32)
+    _, ref = build_both(case, a32, construction)
+    compare_context_sets(case, ref, construction)
+    if construction == "global":
+        assert np.array_equal(case.sets.g.cpu().numpy(), oracle.global_scores_f32(a32))
+    for mode, cm in (("union", relaxkv.CONTEXT_UNION), ("full", relaxkv.CONTEXT_FULL)):
+        for l in range(case.L):
+            R_l = ref.R[l]
+            fresh = case.fresh(l, R_l)
+            out, lse = case.gpu_attn(l, fresh, len(R_l), cm)
+            O_ref, lse_ref = case.oracle_attn(l, ref, fresh, mode=mode)
+            _compare_attn(case, out, lse, O_ref, lse_ref, f"{name} {construction} {mode} {l}")
+
+
+def test_context_variant_then_union_again(gpu_lib):
+    """A later relaxkv_build_sets restores the union context for attention."""
+    case = Case(SMALL["qwen-planted"])
+    a32 = synthetic_scores(case.L, case.T, seed=51)
+    build_both(case, a32, "layerwise")
+    case.req.build_sets(case.sets)
+    assert case.sets.s.context_sets == relaxkv.CONTEXT_SETS_UNION
+    anchors = oracle.select(a32.astype(np.float64), case.k)
+    ref = oracle.build_sets(anchors, case.T)
+    R_l = ref.R[1]
+    fresh = case.fresh(1, R_l)
+    out, lse = case.gpu_attn(1, fresh, len(R_l))
+    O_ref, lse_ref = case.oracle_attn(1, ref, fresh)
+    _compare_attn(case, out, lse, O_ref, lse_ref, "union after layerwise")
+
+
+@pytest.mark.parametrize("construction", ["global", "layerwise"])
+def test_full_size_context_variants(gpu_lib, construction):
+    """The 32K planted workload with seeded fp32 scores: sets bit-exact and
+    attention on sampled targets of sampled layers, in the benchmark's launch
+    configuration."""
+    w = W["qwen14b-32k-planted"]
+    case = Case(w)
+    a32 = synthetic_scores(w.L, w.T_c, seed=52)
+    _, ref = build_both(case, a32, construction)
+    compare_context_sets(case, ref, construction)
+    rng = np.random.default_rng(53)
+    for l in (0, w.L - 1):
+        R_l = ref.R[l]
+        n = len(R_l)
+        fresh = case.fresh(l, R_l)
+        out, lse = case.gpu_attn(l, fresh, n)
+        ts = sorted(set([0, 1, n // 2, n - 1] + rng.integers(0, n, size=6).tolist()))
+        O_ref, lse_ref = case.oracle_attn(l, ref, fresh, targets=ts)
+        _compare_attn(case, out[ts], lse[ts], O_ref, lse_ref, f"32K {construction} layer {l}")

@@ -200,6 +200,21 @@ def test_compute_calls_reject_before_launch(rk):
     assert bg(ctypes.byref(other), ctypes.byref(s), fake, fake, None) == rk.EINVAL
     assert bg(ctypes.byref(p), None, fake, fake, None) == rk.EINVAL
     assert s.global_targets == 0                     # unchanged by rejected calls
+    # build_sets_context (context-construction variants)
+    bc = lib.relaxkv_build_sets_context
+    for c in (-1, 3):
+        assert bc(ctypes.byref(p), fake, c, ctypes.byref(s), None) == rk.EINVAL
+    assert bc(ctypes.byref(p), None, 1, ctypes.byref(s), None) == rk.EINVAL
+    assert bc(ctypes.byref(other), fake, 1, ctypes.byref(s), None) == rk.EINVAL
+    assert bc(ctypes.byref(p), fake, 1, None, None) == rk.EINVAL
+    s3 = _bound_sets(rk, p)
+    s3.ctx = None
+    assert bc(ctypes.byref(p), fake, 1, ctypes.byref(s3), None) == rk.EINVAL
+    s3 = _bound_sets(rk, p)
+    s3.context_sets = 7                              # a corrupted flag is refused
+    assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s3), 0, *args, 0,
+                                   None) == rk.EINVAL
+    assert s.context_sets == 0
     # counts_to_host
     c = (ctypes.c_int32 * 6)()
     assert lib.relaxkv_counts_to_host(None, c, None, None) == rk.EINVAL
