@@ -25,6 +25,10 @@ with Sparse Context Attention for Efficient KV Cache Reuse"):
                       ``mode="full"``.
 * ``update_cache`` -- Sec. 3.4 cache-update semantics, Algorithm 1 update step:
                       fresh rows of R_l overwrite their cache positions.
+* ``query_attn``   -- the query prefill after repair (App. C.4, cache-ready TTFT
+                      protocol): query tokens attend to the cache and causally
+                      to themselves; its row log-sum-exp is the normaliser of
+                      the supplied-LSE scoring mode.
 * ``build_sets_context`` -- the context-construction variants of Sec. 4.4
                       (Global Sparse, Layerwise Sparse): the same anchors and
                       targets with the context set U_l replaced.
@@ -427,6 +431,49 @@ def attention_flops(H, d, edges):
     per edge and query head one d-long dot product (2d) and one d-long
     weighted sum (2d)."""
     return 4.0 * H * d * float(np.sum(edges))
+
+
+# ----------------------------------------------------------------------------
+# Query-side completion: the query prefill of the cache-ready TTFT protocol
+# (App. C.4): the query tokens attend to the (repaired) cache and causally to
+# themselves.
+# ----------------------------------------------------------------------------
+
+def query_attn(q_l, k_cache_l, v_cache_l, k_q, v_q, softmax_scale=None):
+    """Attention of the n_query query tokens of one layer, placed after the T_c
+    context positions: token t attends to every cache position 0..T_c-1 and to
+    the query tokens 0..t.
+
+    q_l [n_query][H][d]; k_cache_l / v_cache_l [H_kv][T_c][d] (the layer's cache,
+    naive or repaired); k_q / v_q [n_query][H_kv][d] (the query tokens' own keys
+    and values).  Returns (O [n_query][H][d], lse [n_query][H]) in float64; lse
+    is the natural-log normaliser over all keys a row sees, the value the
+    supplied-LSE scoring mode takes as q_lse.
+    """
+    q_l = np.asarray(q_l, dtype=np.float64)
+    k_cache_l = np.asarray(k_cache_l, dtype=np.float64)
+    v_cache_l = np.asarray(v_cache_l, dtype=np.float64)
+    k_q = np.asarray(k_q, dtype=np.float64)
+    v_q = np.asarray(v_q, dtype=np.float64)
+    Qn, H, d = q_l.shape
+    H_kv, T_c, _ = k_cache_l.shape
+    G = H // H_kv
+    sigma = 1.0 / np.sqrt(d) if softmax_scale is None else float(softmax_scale)
+    O = np.zeros((Qn, H, d))
+    lse = np.zeros((Qn, H))
+    for h in range(H):
+        g = h // G
+        K = np.concatenate([k_cache_l[g], k_q[:, g, :]], axis=0)    # [T_c + Qn][d]
+        V = np.concatenate([v_cache_l[g], v_q[:, g, :]], axis=0)
+        for t in range(Qn):
+            m = T_c + t + 1                                          # keys visible to token t
+            s = sigma * (K[:m] @ q_l[t, h])
+            mx = s.max()
+            e = np.exp(s - mx)
+            z = e.sum()
+            O[t, h] = (e / z) @ V[:m]
+            lse[t, h] = mx + np.log(z)
+    return O, lse
 
 
 # ----------------------------------------------------------------------------

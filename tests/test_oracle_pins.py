@@ -684,3 +684,51 @@ def test_attention_context_variants_brute_force(construction, mode):
                 ref = sum(wi * vj for wi, (_, vj) in zip(w, terms)) / math.fsum(w)
                 np.testing.assert_allclose(O[t, hh], ref, atol=1e-12)
                 assert lse[t, hh] == pytest.approx(m + math.log(math.fsum(w)), abs=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# query-side completion: query tokens over the cache and causally over themselves
+# ----------------------------------------------------------------------------
+
+def test_query_attn_matches_sdpa_with_offset_causal_mask():
+    from oracle import query_attn
+    rng = np.random.default_rng(60)
+    T, Qn, H, H_kv, d = 23, 6, 6, 2, 16
+    q = rng.standard_normal((Qn, H, d))
+    kc, vc = rng.standard_normal((H_kv, T, d)), rng.standard_normal((H_kv, T, d))
+    kq, vq = rng.standard_normal((Qn, H_kv, d)), rng.standard_normal((Qn, H_kv, d))
+    O, lse = query_attn(q, kc, vc, kq, vq)
+    K = torch.cat([torch.from_numpy(kc), torch.from_numpy(kq).permute(1, 0, 2)], dim=1)   # [H_kv][T+Qn][d]
+    V = torch.cat([torch.from_numpy(vc), torch.from_numpy(vq).permute(1, 0, 2)], dim=1)
+    mask = torch.arange(T + Qn)[None, :] <= (T + torch.arange(Qn))[:, None]               # [Qn][T+Qn]
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q).permute(1, 0, 2)[None], K[None], V[None], attn_mask=mask,
+        enable_gqa=True)
+    np.testing.assert_allclose(O, ref[0].permute(1, 0, 2).numpy(), atol=1e-12)
+    Kh = K.repeat_interleave(H // H_kv, dim=0)                                             # [H][T+Qn][d]
+    logits = torch.einsum("htd,hkd->htk", torch.from_numpy(q).permute(1, 0, 2), Kh) / math.sqrt(d)
+    logits = logits.masked_fill(~mask[None], float("-inf"))
+    np.testing.assert_allclose(lse, torch.logsumexp(logits, -1).permute(1, 0).numpy(), atol=1e-12)
+
+
+def test_query_attn_brute_force_and_normalisation():
+    from oracle import query_attn
+    rng = np.random.default_rng(61)
+    T, Qn, H, H_kv, d = 9, 4, 2, 1, 4
+    q = rng.standard_normal((Qn, H, d))
+    kc, vc = rng.standard_normal((H_kv, T, d)), rng.standard_normal((H_kv, T, d))
+    kq, vq = rng.standard_normal((Qn, H_kv, d)), rng.standard_normal((Qn, H_kv, d))
+    O, lse = query_attn(q, kc, vc, kq, vq, softmax_scale=0.3)
+    for t in range(Qn):
+        for h in range(H):
+            keys = [kc[0, j] for j in range(T)] + [kq[u, 0] for u in range(t + 1)]
+            vals = [vc[0, j] for j in range(T)] + [vq[u, 0] for u in range(t + 1)]
+            x = [0.3 * float(np.dot(q[t, h], k)) for k in keys]
+            z = math.fsum(math.exp(v) for v in x)
+            assert lse[t, h] == pytest.approx(math.log(z), abs=1e-12)
+            ref = sum(math.exp(xi) / z * vi for xi, vi in zip(x, vals))
+            np.testing.assert_allclose(O[t, h], ref, atol=1e-12)
+            # the cache keys' share plus the query prefix's share is 1
+            cache_mass = math.fsum(math.exp(xi - lse[t, h]) for xi in x[:T])
+            prefix_mass = math.fsum(math.exp(xi - lse[t, h]) for xi in x[T:])
+            assert cache_mass + prefix_mass == pytest.approx(1.0, abs=1e-12)
