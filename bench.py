@@ -249,6 +249,39 @@ def time_context_variants(b: Bench, reps=2):
     return res
 
 
+def time_query_attn(b: Bench, reps=3):
+    """Query-side completion: the query tokens' attention over each layer's
+    cache and causally over themselves (per-layer launches, as a query prefill
+    runs them), with the row LSE.  HBM bytes per layer: the layer's K and V
+    cache plus the query rows, their keys/values and the outputs."""
+    w = b.w
+    req = b.req
+    kvq = [synth.make_query_kv(w, l, "cuda") for l in range(w.L)]
+    out = torch.empty(w.Qn, w.H, w.d, dtype=b.q.dtype, device="cuda")
+    lse = torch.empty(w.Qn, w.H, dtype=torch.float32, device="cuda")
+    ws = req.alloc_query_workspace()
+    mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    times = []
+    for i in range(reps + 1):
+        e0, e1 = mk(), mk()
+        e0.record()
+        for l in range(w.L):
+            req.query_attn(l, b.kc, b.vc, *kvq[l], out, lse, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        if i:
+            times.append(e0.elapsed_time(e1))
+    ms = float(np.mean(times))
+    esz = 2 if w.dtype == "bf16" else 4
+    nbytes = esz * (2 * w.H_kv * w.T_c * w.d + 2 * w.Qn * w.H * w.d + 2 * w.Qn * w.H_kv * w.d) \
+        + 4 * w.Qn * w.H
+    us = 1e3 * ms / w.L
+    return {"us_per_layer": us, "gbs": nbytes / (us * 1e-6) / 1e9,
+            "hbm_frac": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+            "bytes_per_layer": nbytes,
+            "tflops": 4.0 * w.H * w.d * w.Qn * (w.T_c + (w.Qn + 1) / 2) / (us * 1e-6) / 1e12}
+
+
 def time_scoring_supplied_lse(b: Bench, reps=5):
     """Time relaxkv_score in its one-pass mode: each query row's log-sum-exp is
     supplied, as the query's own forward pass would produce it (computed here
@@ -340,8 +373,9 @@ def main():
                     help="also time the Full-Prefix Control on the same targets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-matched-targets", action="store_true",
-                    help="skip the global-target sweep point and the context-construction "
-                         "variants (profiles of the main path's attention launches only)")
+                    help="skip the global-target sweep point, the context-construction "
+                         "variants and the query-side completion (profiles of the main "
+                         "path's attention launches only)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run one plain device-to-device copy of MIB MiB (reference "
                          "kernel for scaling the HBM byte counters) and exit")
@@ -409,6 +443,7 @@ def main():
     if not args.no_matched_targets:
         res["matched_targets"] = time_matched_targets(b)
         res["context_variants"] = time_context_variants(b)
+        res["query_attn"] = time_query_attn(b)
     if args.control:
         rc = b.timed(args.steps, args.warmup, mode=relaxkv.CONTEXT_FULL)
         res["control"] = {"attn_ms_full_prefix": rc["attn_ms_total"],

@@ -17,8 +17,10 @@
  * plus the cache update of the repaired rows (relaxkv_update_cache, Sec. 3.4)
  * the matched-target variants, where one global target list replaces R_l
  * (relaxkv_select_global, relaxkv_build_sets_global; Sec. 4.1, App. A.3, App. B),
- * and the context-construction variants, where another context set of the same
- * size replaces U (relaxkv_build_sets_context; Sec. 4.4).
+ * the context-construction variants, where another context set of the same
+ * size replaces U (relaxkv_build_sets_context; Sec. 4.4), and the query-side
+ * completion: the query tokens' attention over the repaired cache, whose row
+ * log-sum-exp feeds the one-pass scoring mode (relaxkv_query_attn; App. C.4).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -318,6 +320,35 @@ relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets*
 relaxkv_status relaxkv_update_cache(const relaxkv_problem* p, const relaxkv_sets* s,
                                     int32_t layer, const void* k_new, const void* v_new,
                                     void* k_cache, void* v_cache, void* stream);
+
+/* Host only.  Device scratch bytes relaxkv_query_attn needs (0 for float32
+ * problems, which need none; 0 when p is invalid). */
+size_t relaxkv_query_attn_workspace_bytes(const relaxkv_problem* p);
+
+/*
+ * Query-side completion of layer `layer` (the query prefill of App. C.4's
+ * cache-ready TTFT protocol, after repair): the n_query query tokens, placed
+ * after the T_c context positions, attend to every cache position and causally
+ * to themselves:
+ *   O_{t,h} = sum_j softmax_j(sigma <q_{l,t,h}, K_j>) V_j,  j over the cache
+ *   positions 0..T_c-1 and then the query tokens 0..t, KV head h / (H / H_kv).
+ * The queries are the layer's rows of p->q.
+ *   k_cache, v_cache  device [L][H_kv][T_c][d] in dtype: the cache to attend to (the
+ *                     naive cache, or one repaired by relaxkv_update_cache); layer
+ *                     `layer` is read.
+ *   k_q, v_q          device [n_query][H_kv][d] in dtype: the query tokens' own keys
+ *                     and values at this layer.
+ *   out               device out [n_query][H][d] in dtype.
+ *   lse_out           optional device out [n_query][H] float32: the natural-log
+ *                     normaliser of each row over all keys it sees, the value
+ *                     relaxkv_score takes as q_lse (layer row l).
+ *   ws                device scratch of ws_bytes >= relaxkv_query_attn_workspace_bytes(p)
+ *                     (may be NULL when that is 0).
+ */
+relaxkv_status relaxkv_query_attn(const relaxkv_problem* p, int32_t layer, const void* k_cache,
+                                  const void* v_cache, const void* k_q, const void* v_q,
+                                  void* out, float* lse_out, void* ws, size_t ws_bytes,
+                                  void* stream);
 
 /*
  * Synchronising.  Copies s->counts ([L+2] int32) to host_counts and, when

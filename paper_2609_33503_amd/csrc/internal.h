@@ -24,6 +24,19 @@ struct ScoreWorkspace {
 
 ScoreWorkspace score_workspace_layout(const relaxkv_problem& p);
 
+// Scratch layout of relaxkv_query_attn (bf16 path; the fp32 path needs none).
+struct QueryAttnWorkspace {
+    size_t part_o_off;  // bf16 [n_split][H_kv][rows_pad][d] normalised partial outputs
+    size_t part_l_off;  // float [n_split][H_kv][rows_pad] log2-sum-exp of each partial
+    size_t total;
+    int n_split;        // cache-key splits (the last also takes the query tokens' keys)
+    int kps;            // cache keys per split (a multiple of 64)
+    int n_chunks;       // row chunks of up to 320 rows per KV head
+    int rows_pad;       // n_query * G rounded up to a multiple of 32
+};
+
+QueryAttnWorkspace query_attn_workspace_layout(const relaxkv_problem& p);
+
 // Kernel launchers (each returns hipSuccess or the launch error).
 hipError_t launch_score(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws,
                         float* scores, hipStream_t st);
@@ -46,6 +59,9 @@ hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s,
 hipError_t launch_update_cache(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
                                const void* k_new, const void* v_new, void* k_cache,
                                void* v_cache, hipStream_t st);
+hipError_t launch_query_attn(const relaxkv_problem& p, int layer, const void* k_cache,
+                             const void* v_cache, const void* k_q, const void* v_q, void* out,
+                             float* lse_out, char* ws, hipStream_t st);
 hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
                               const void* q_new, const void* k_new, const void* v_new,
                               void* out, float* lse_out, int context_mode, hipStream_t st);

@@ -239,6 +239,26 @@ relaxkv_status relaxkv_update_cache(const relaxkv_problem* p, const relaxkv_sets
                                         (hipStream_t)stream));
 }
 
+size_t relaxkv_query_attn_workspace_bytes(const relaxkv_problem* p) {
+    if (relaxkv_validate(p) != RELAXKV_OK) return 0;
+    return query_attn_workspace_layout(*p).total;
+}
+
+relaxkv_status relaxkv_query_attn(const relaxkv_problem* p, int32_t layer, const void* k_cache,
+                                  const void* v_cache, const void* k_q, const void* v_q,
+                                  void* out, float* lse_out, void* ws, size_t ws_bytes,
+                                  void* stream) {
+    relaxkv_status st = relaxkv_validate(p);
+    if (st != RELAXKV_OK) return st;
+    if (layer < 0 || layer >= p->L) return RELAXKV_EINVAL;
+    if (!k_cache || !v_cache || !k_q || !v_q || !out) return RELAXKV_EINVAL;
+    const QueryAttnWorkspace w = query_attn_workspace_layout(*p);
+    if (w.total && !ws) return RELAXKV_EINVAL;
+    if (ws_bytes < w.total) return RELAXKV_ENOSPACE;
+    return from_hip(launch_query_attn(*p, layer, k_cache, v_cache, k_q, v_q, out, lse_out,
+                                      (char*)ws, (hipStream_t)stream));
+}
+
 relaxkv_status relaxkv_counts_to_host(const relaxkv_sets* s, int32_t* host_counts,
                                       int64_t* host_edges, void* stream) {
     if (!s || !s->counts || !s->edges || !host_counts || s->L < 1) return RELAXKV_EINVAL;

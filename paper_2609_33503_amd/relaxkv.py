@@ -27,7 +27,7 @@ EXPORTS = ("relaxkv_status_string", "relaxkv_anchor_count", "relaxkv_validate",
            "relaxkv_score", "relaxkv_select", "relaxkv_build_sets", "relaxkv_build_sets_context",
            "relaxkv_select_global",
            "relaxkv_build_sets_global", "relaxkv_sparse_attn", "relaxkv_update_cache",
-           "relaxkv_counts_to_host")
+           "relaxkv_query_attn_workspace_bytes", "relaxkv_query_attn", "relaxkv_counts_to_host")
 
 
 class RelaxKVError(RuntimeError):
@@ -99,6 +99,11 @@ def load(path=None):
     lib.relaxkv_update_cache.restype = c_int32
     lib.relaxkv_update_cache.argtypes = [POINTER(Problem), POINTER(Sets), c_int32, c_void_p,
                                          c_void_p, c_void_p, c_void_p, c_void_p]
+    lib.relaxkv_query_attn_workspace_bytes.restype = c_size_t
+    lib.relaxkv_query_attn_workspace_bytes.argtypes = [POINTER(Problem)]
+    lib.relaxkv_query_attn.restype = c_int32
+    lib.relaxkv_query_attn.argtypes = [POINTER(Problem), c_int32, c_void_p, c_void_p, c_void_p,
+                                       c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     lib.relaxkv_counts_to_host.restype = c_int32
     lib.relaxkv_counts_to_host.argtypes = [POINTER(Sets), POINTER(c_int32), POINTER(c_int64),
                                            c_void_p]
@@ -254,6 +259,27 @@ class Request:
                                            _ptr(k_new), _ptr(v_new), _ptr(k_cache),
                                            _ptr(v_cache), _stream(stream)),
                "relaxkv_update_cache")
+
+
+    # ---- query-side completion (the query prefill after repair)
+    def query_attn_workspace_bytes(self):
+        return load().relaxkv_query_attn_workspace_bytes(ctypes.byref(self.p))
+
+    def alloc_query_workspace(self):
+        n = self.query_attn_workspace_bytes()
+        return None if n == 0 else torch.empty(n, dtype=torch.uint8, device=self.tensors[1].device)
+
+    def query_attn(self, layer, k_cache, v_cache, k_q, v_q, out, lse_out=None, ws=None,
+                   stream=None):
+        """k_cache/v_cache [L][H_kv][T_c][d]; k_q/v_q [n_query][H_kv][d]; out [n_query][H][d]."""
+        for t in (k_cache, v_cache, k_q, v_q, out):
+            if not t.is_contiguous() or t.dtype != self.dtype:
+                raise ValueError("caches, query keys/values and out must be contiguous, "
+                                 "in the problem dtype")
+        _check(load().relaxkv_query_attn(ctypes.byref(self.p), int(layer), _ptr(k_cache),
+                                         _ptr(v_cache), _ptr(k_q), _ptr(v_q), _ptr(out),
+                                         _ptr(lse_out), _ptr(ws), 0 if ws is None else ws.numel(),
+                                         _stream(stream)), "relaxkv_query_attn")
 
 
 class SetsBuffer:

@@ -25,6 +25,7 @@ Layouts (row-major, last index contiguous):
   q_new     [T_c][H][d]       fresh queries for every context position
   k_new     [T_c][H_kv][d]    fresh keys   = cached + sigma_p * N(0, 1)
   v_new     [T_c][H_kv][d]    fresh values = cached + sigma_p * N(0, 1)
+  k_q, v_q  [Qn][H_kv][d]     the query tokens' own keys and values (law of K, V)
 The harness gathers the rows of the active targets out of the fresh tensors
 (``gather_rows``); in a real model they would be the projections' outputs.
 """
@@ -39,7 +40,7 @@ import torch
 
 BASE_SEED = 42                 # the paper's random seed (App. C.1)
 _GLOBAL = 65535                # spawn-key "layer" slot for per-workload streams
-_T_Q, _T_K, _T_V, _T_QN, _T_KN, _T_VN, _T_PLANT = range(7)
+_T_Q, _T_K, _T_V, _T_QN, _T_KN, _T_VN, _T_PLANT, _T_QK, _T_QV = range(9)
 
 
 @dataclass(frozen=True)
@@ -157,6 +158,15 @@ def make_fresh_layer(w: Workload, layer: int, k_cache, v_cache, device="cpu"):
     kn = (kc + w.sigma_p * _normal((w.T_c, w.H_kv, w.d), w.wid, layer, _T_KN, device)).to(dt)
     vn = (vc + w.sigma_p * _normal((w.T_c, w.H_kv, w.d), w.wid, layer, _T_VN, device)).to(dt)
     return qn, kn.contiguous(), vn.contiguous()
+
+
+def make_query_kv(w: Workload, layer: int, device="cpu"):
+    """(k_q, v_q) [Qn][H_kv][d] of one layer: the user-query tokens' own keys and
+    values, drawn with the law of the cached K and V."""
+    dt = w.torch_dtype
+    kq = (_normal((w.Qn, w.H_kv, w.d), w.wid, layer, _T_QK, device) * w.std).to(dt)
+    vq = (_normal((w.Qn, w.H_kv, w.d), w.wid, layer, _T_QV, device) * w.std).to(dt)
+    return kq.contiguous(), vq.contiguous()
 
 
 def gather_rows(t, rows):

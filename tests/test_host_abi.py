@@ -215,6 +215,23 @@ def test_compute_calls_reject_before_launch(rk):
     assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s3), 0, *args, 0,
                                    None) == rk.EINVAL
     assert s.context_sets == 0
+    # query_attn (query-side completion)
+    qws = lib.relaxkv_query_attn_workspace_bytes(ctypes.byref(p))
+    assert qws > 0 and qws % 256 == 0
+    qa = lib.relaxkv_query_attn
+    for layer in (-1, 4):
+        assert qa(ctypes.byref(p), layer, fake, fake, fake, fake, fake, None, fake, qws,
+                  None) == rk.EINVAL
+    for i in range(5):
+        ptrs = [fake] * 5
+        ptrs[i] = None
+        assert qa(ctypes.byref(p), 0, *ptrs, None, fake, qws, None) == rk.EINVAL
+    assert qa(ctypes.byref(p), 0, fake, fake, fake, fake, fake, None, None, qws, None) == rk.EINVAL
+    assert qa(ctypes.byref(p), 0, fake, fake, fake, fake, fake, None, fake, qws - 1,
+              None) == rk.ENOSPACE
+    assert qa(ctypes.byref(_problem(rk, d=96)), 0, fake, fake, fake, fake, fake, None, fake, qws,
+              None) == rk.EUNSUPPORTED
+    assert lib.relaxkv_query_attn_workspace_bytes(ctypes.byref(_problem(rk, d=96))) == 0
     # counts_to_host
     c = (ctypes.c_int32 * 6)()
     assert lib.relaxkv_counts_to_host(None, c, None, None) == rk.EINVAL
