@@ -7,25 +7,26 @@
 //
 // bf16 kernel (bf16 MFMA 32x32x16, fp32 accumulation, flash-style online
 // softmax in the exp2 domain):
-// - a workgroup of 4 waves owns 128 (target, head) rows of one KV head g:
-//   floor(128/G) consecutive targets times the G query heads that share g, so
-//   every gathered K/V tile is used by all G heads;
-// - per tile of 64 context keys the 256 threads gather the K and V rows into
-//   LDS, choosing per key between the fresh rows (k_new/v_new) and the cached
-//   layer (k_cache/v_cache); K is stored row-major, V transposed so the PV
-//   product reads it as an MFMA A operand;
+// - a workgroup of NW = 12 waves owns NW*32 (target, head) rows of one KV head
+//   g: floor(NW*32/G) consecutive targets times the G query heads that share g,
+//   so every K/V row brought into LDS is used by all G heads of NW*32/G targets;
+// - context keys go in steps of 64 through a 4-deep ring of LDS buffers (a K
+//   and a V tile per step, unpadded rows with an XOR swizzle), filled by direct
+//   global->LDS loads that choose per key between the fresh rows
+//   (k_new/v_new) and the cached layer; the keys' indices (U and src, or rank)
+//   are staged into LDS the same way one step earlier, so the only vector
+//   loads in flight are LDS fills, waited for by in-order counts;
 // - each wave computes S^T = K Q^T with one query row per lane (Q stays in
 //   registers), so row max and row sum are lane-local plus one exchange with
-//   the lane 32 away; P^T stays in registers as the B operand of O^T = V^T P^T;
-// - the mask is the staircase of the targets' limits: tiles below the first
+//   the lane 32 away; P^T stays in registers as the B operand of
+//   O^T = V^T P^T, whose V^T operand comes from transposing LDS reads;
+// - the mask is the staircase of the targets' limits: steps below the first
 //   target's limit run unmasked, the rest compare each key with its row's limit;
 // - tiles are taken heaviest-first (the last targets have the longest
 //   contexts) and consecutive workgroups cycle through the KV heads, so the
-//   workgroups that land on one XCD share a KV head and its L2 working set;
-// - the global loads of the next tile are issued before the current tile's
-//   MFMAs.
+//   workgroups that land on one XCD share a KV head and its L2 working set.
 // fp32 kernel: one wave per (target, head), VALU dot products and an online
-// softmax across the wave; used for fp32 inputs where bf16 MFMA would not meet
+// softmax across the wave; used for fp32 inputs, where bf16 MFMA would not meet
 // fp32 accuracy.
 
 #include <math.h>
@@ -77,7 +78,6 @@ __device__ __forceinline__ size_t kv_row(const AttnArgs& a, int c, int g, bool& 
 constexpr float kRescaleSlack = 8.0f;      // log2 units the running max may lag the true max
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
-typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 // max / sum of a value and its copy in the lane 32 away (one VALU swap).
@@ -90,21 +90,23 @@ __device__ __forceinline__ float pair_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// NW waves x RB*32 rows per workgroup; LDS tiles of BN keys, computed in
-// 64-key steps of two 32-key MFMA blocks.  With RB = 2 every K and V fragment
-// read from LDS feeds two MFMAs (one per 32-row block).
-template <int D, bool FULL, int NW, int BN, int RB>
-__global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(AttnArgs a) {
-    constexpr int NT = NW * 64;            // threads
+// NW waves of 32 rows, 64-key steps, one barrier per step.  The fills of step
+// j+3 and the indices of step j+4 are issued right after the barrier of step j,
+// so every fill has two steps of compute to land.
+template <int D, bool FULL, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
+    constexpr int TK = 64, NST = 4;
     constexpr int KS = D / 16;             // k-steps of the QK^T contraction
     constexpr int DB = D / 32;             // 32-wide d blocks of O^T
-    constexpr int KSTR = D + 8;            // K tile row stride (elements)
-    constexpr int VSTR = D + RELAXKV_ATTN_VPAD;   // V tile row stride (elements)
-    constexpr int P = D / 8;               // 16-byte parts per row
-    constexpr int KPT = BN * P / NT;       // keys per thread in the loader
-    static_assert(KPT >= 1 && BN * P == KPT * NT, "loader shape");
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BN * KSTR];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][BN * VSTR];
+    constexpr int ROWB = 2 * D;            // tile row bytes
+    constexpr int CH = D / 8;              // 16-byte chunks per row
+    constexpr int RPI = 64 / CH;           // rows per wave-wide load
+    constexpr int NL = TK / RPI;           // wave-wide loads per step and tensor
+    constexpr int PPW = (NL + NW - 1) / NW;   // K/V load pairs of the busiest wave
+    constexpr int NWAIT = 2 * PPW;         // its fills per step
+    __shared__ __attribute__((aligned(1024))) uint16_t Kt[NST][TK * D];
+    __shared__ __attribute__((aligned(1024))) uint16_t Vt[NST][TK * D];
+    __shared__ __attribute__((aligned(256))) int32_t Ix[NST][2][TK];   // [U or rank, src]
 
     const int Hkv = a.Hkv;
     const int g = blockIdx.x % Hkv;
@@ -117,268 +119,210 @@ __global__ __launch_bounds__(NW * 64, RB == 1 ? 8 / NW : 4 / NW) void attn_bf16(
     const int t1 = min(t0 + a.BT, nR);
     const int off = a.R_off[a.layer];
     const int32_t* lim_of = FULL ? a.R_idx + off : a.R_u + off;
-    // Limits are compact indices (union) or positions (full prefix).  A global
-    // target that precedes every union position has limit -1 (empty context):
-    // its row masks every key and is written as the empty sum at the end.
     const int cmin = lim_of[t0];
     const int cmax = max(lim_of[t1 - 1], 0);
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, hf = lane >> 5;
-    const uint16_t* qn = (const uint16_t*)a.q_new;
-    const float sl2 = a.scale * kLog2e;              // > 0
+    const float sl2 = a.scale * kLog2e;
 
-    // This lane's (target, head) rows, one per 32-row block.
-    int t_of[RB], head_of[RB], lim[RB];
-    bool valid[RB];
-    bf16x8 qf[RB][KS];
-    f32x16 o[RB][DB];
-    float m_run[RB], l_run[RB];
+    const int rho = w * 32 + r32;
+    const int tl = rho / a.G, hh = rho - tl * a.G;
+    const int t_row = t0 + tl;
+    const bool valid = tl < a.BT && t_row < t1;
+    const int lim_v = lim_of[valid ? t_row : t0];   // value select: no pointer to cmax
+    const int lim = valid ? lim_v : cmax;
+    const int head = g * a.G + hh;
+    bf16x8 qf[KS];
+    {
+        const uint16_t* qrow = (const uint16_t*)a.q_new +
+                               ((size_t)(valid ? t_row : t0) * a.H + (valid ? head : 0)) * D;
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        const int rho = (w * RB + rb) * 32 + r32;
-        const int tl = rho / a.G, hh = rho - tl * a.G;
-        t_of[rb] = t0 + tl;
-        valid[rb] = tl < a.BT && t_of[rb] < t1;
-        lim[rb] = valid[rb] ? lim_of[t_of[rb]] : cmax;   // padding rows: finite, never stored
-        head_of[rb] = g * a.G + hh;
-        const uint16_t* qrow =
-            qn + ((size_t)(valid[rb] ? t_of[rb] : t0) * a.H + (valid[rb] ? head_of[rb] : 0)) * D;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qf[rb][ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) o[rb][db] = f32x16{};
-        m_run[rb] = lim[rb] < 0 ? 0.f : -INFINITY;     // empty context: every p is exp2(-inf) = 0
-        l_run[rb] = 0.f;
+        for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
     }
+    f32x16 o[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = f32x16{};
+    float m_run = lim < 0 ? 0.f : -INFINITY;       // empty context: every p is exp2(-inf) = 0
+    float l_run = 0.f;
 
-    // Loader: thread -> (key group kq, 16-byte part); keys kq*KPT .. kq*KPT+KPT-1.
-    // Two-stage pipeline: the row indices of tile kt+2 are loaded while tile kt
-    // is computed; the K/V rows of tile kt+1 are loaded from them one step later.
-    const int kq = tid / P, part = tid % P;
-    const uint16_t* kn = (const uint16_t*)a.k_new;
-    const uint16_t* vn = (const uint16_t*)a.v_new;
-    const uint16_t* kc = (const uint16_t*)a.kc;
-    const uint16_t* vc = (const uint16_t*)a.vc;
+    const uint16_t* kng = (const uint16_t*)a.k_new + (size_t)g * D;     // fresh rows: stride Hkv*D
+    const uint16_t* kcg = (const uint16_t*)a.kc + (size_t)g * a.T * D;  // cached rows: stride D
+    const long dv_fresh = (const uint16_t*)a.v_new - (const uint16_t*)a.k_new;
+    const long dv_cached = (const uint16_t*)a.vc - (const uint16_t*)a.kc;
     const int32_t* srcmap = FULL ? a.rank_l : a.src_l;
-    // Per-workgroup bases of KV head g; per key only a row offset is added.
-    const uint16_t* kng = kn + (size_t)g * D;                    // fresh rows: stride Hkv*D
-    const uint16_t* kcg = kc + (size_t)g * a.T * D;              // cached rows: stride D
-    const long dv_fresh = vn - kn;                               // V address = K address + delta
-    const long dv_cached = vc - kc;
-    int ipos[KPT], irow[KPT];                        // position, fresh rank (-1: cached row)
-    u32x4 kr[KPT], vr[KPT];
+    const int S = cmax / TK + 1;                     // 64-key steps
 
-    // Keys past cmax re-read the row of cmax: their logits are masked (every
-    // 64-key step that holds such a key is a staircase step), so only
-    // finiteness matters.
-    auto load_idx = [&](int c0) {
-#pragma unroll
-        for (int kk = 0; kk < KPT; ++kk) {
-            const int c = min(c0 + kq * KPT + kk, cmax);
-            ipos[kk] = FULL ? c : a.U[c];
-            irow[kk] = srcmap[c];
+    auto issue_idx = [&](int m) {
+        if (w < (FULL ? 1 : 2)) {
+            int ww = w;
+            asm volatile("" : "+s"(ww));
+            const int c = min(m * TK + lane, cmax);
+            const int32_t* src = FULL ? srcmap + c : (ww == 0 ? a.U + c : srcmap + c);
+            fill_lds4(src, lds_addr(&Ix[m & 3][ww][0]));
         }
     };
-    auto load_rows = [&]() {
+    auto issue_rows = [&](int m) {
+        int lr = lane / CH, pc = lane % CH, ww = w;
+        asm volatile("" : "+v"(lr), "+v"(pc), "+s"(ww));
+        const int st = m & 3;
 #pragma unroll
-        for (int kk = 0; kk < KPT; ++kk) {
-            const bool fresh = irow[kk] >= 0;
-            const uint16_t* kp = fresh ? kng + (size_t)irow[kk] * (Hkv * D) : kcg + (size_t)ipos[kk] * D;
-            kp += part * 8;
-            kr[kk] = *(const u32x4*)kp;
-            vr[kk] = *(const u32x4*)(kp + (fresh ? dv_fresh : dv_cached));
+        for (int i = 0; i < PPW; ++i) {
+            const int j = ww + i * NW;
+            if (NL % NW == 0 || j < NL) {
+                const int row = j * RPI + lr;
+                const int c = m * TK + row;
+                const int pos = FULL ? min(c, cmax) : Ix[st][0][row];
+                const int r = Ix[st][FULL ? 0 : 1][row];
+                const bool fresh = r >= 0;
+                const uint16_t* kp = (fresh ? kng + (size_t)r * (Hkv * D) : kcg + (size_t)pos * D) +
+                                     ((pc ^ tile_swz<D>(row)) << 3);
+                const uint16_t* vp = kp + (fresh ? dv_fresh : dv_cached);
+                fill_lds16(kp, lds_addr(Kt[st] + j * RPI * D));
+                fill_lds16(vp, lds_addr(Vt[st] + j * RPI * D));
+            }
         }
     };
 
-    // Transposing V reads: lane (group G = lane/16, j = lane%16) points at key row
-    // 4*(G/2) + j/4 and d column (G%2)*16 + 4*(j%4) of each 16-key, 32-d block.
-    // ds_read_b64_tr_b16 gives lane i of a 16-lane group element i%4 of the
-    // 8-byte chunks read by lanes 4m + i/4 (m = 0..3), so lane i receives 4 keys
-    // at one d: element e of the k-index block hf*8 .. hf*8+7 of half k2 is key
-    // 16*k2 + 8(e/4) + 4hf + e%4 of the 32-key block, the S^T lane layout.
-    const int vtr_off = (4 * (lane >> 5) + ((lane & 15) >> 2)) * VSTR + ((lane >> 4) & 1) * 16 +
-                        4 * (lane & 3);
+    const int k_base = r32 * ROWB | ((hf ^ tile_swz<D>(r32)) << 4);
+    const int rl = 4 * (lane >> 5) + ((lane & 15) >> 2);
+    const int cl = ((lane >> 4) & 1) * 2 + ((lane & 3) >> 1);
+    const int v_base0 = rl * ROWB | ((cl ^ tile_swz<D>(rl)) << 4) | ((lane & 1) << 3);
+    const int v_base1 = (rl + 8) * ROWB | ((cl ^ tile_swz<D>(rl + 8)) << 4) | ((lane & 1) << 3);
 
-    const int nkt = cmax / BN + 1;
-    load_idx(0);
-    load_rows();
-    if (nkt > 1) load_idx(BN);
-    for (int kt = 0; kt < nkt; ++kt) {
-        uint16_t* ks_b = Ks[kt & 1];
-        uint16_t* vs_b = Vs[kt & 1];
-        // Store tile kt.  The buffer was last read in step kt-2, which every wave
-        // finished before the barrier of step kt-1.
 #pragma unroll
-        for (int kk = 0; kk < KPT; ++kk) {
-            *(u32x4*)(ks_b + (kq * KPT + kk) * KSTR + part * 8) = kr[kk];
-            *(u32x4*)(vs_b + (kq * KPT + kk) * VSTR + part * 8) = vr[kk];
-        }
-        __syncthreads();
-        if (kt + 1 < nkt) {
-            load_rows();                                   // tile kt+1
-            if (kt + 2 < nkt) load_idx((kt + 2) * BN);     // indices of tile kt+2
-        }
+    for (int m = 0; m < NST; ++m)
+        if (m < S) issue_idx(m);
+    wait_loads_barrier<0>();
 #pragma unroll
-        for (int sub = 0; sub < BN / 64; ++sub) {
-            const int c0 = kt * BN + sub * 64;
-            if (c0 > cmax) break;
-            const uint16_t* kst = ks_b + sub * 64 * KSTR;
-            const uint16_t* vst = vs_b + sub * 64 * VSTR;
-            // S^T = K Q^T: s[rb][kb][v] = S[row rb][key c0 + kb*32 + 8(v/4) + 4hf + v%4]
-            f32x16 s[RB][2];
+    for (int m = 0; m < NST - 1; ++m)
+        if (m < S) issue_rows(m);
+
+    for (int j = 0; j < S; ++j) {
+        // The fills of step j and the indices of step j+3 are complete (only the
+        // fills of step j+2 may be in flight), and every wave is done with step
+        // j-1, whose buffers the fills of step j+3 reuse.
+        wait_loads_barrier<NWAIT>();
+        if (j + NST < S) issue_idx(j + NST);
+        if (j + NST - 1 < S) issue_rows(j + NST - 1);
+        // S^T = K Q^T: s[kb][v] = S[row][key 64 j + 32 kb + 8(v/4) + 4 hf + v%4]
+        f32x16 s[2];
+        {
+            int kbo = k_base;
+            asm volatile("" : "+v"(kbo));
+            const char* kst = (const char*)Kt[j & 3];
+            s[0] = s[1] = f32x16{};
+            // K fragments x = 2 ks + kb, read KA ahead of their MFMA.
+            constexpr int KA = RELAXKV_ATTN_KAHEAD < 2 * KS ? RELAXKV_ATTN_KAHEAD : 2 * KS;
+            auto frag = [&](int x) {
+                return *(const bf16x8*)(kst + (x & 1) * 32 * ROWB + (kbo ^ ((x >> 1) << 5)));
+            };
+            bf16x8 kf[KA];
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x16{};
+            for (int x = 0; x < KA; ++x) kf[x] = frag(x);
 #if RELAXKV_ATTN_SETPRIO
             __builtin_amdgcn_s_setprio(2);
 #endif
-            // K fragments are read ahead of the MFMAs that use them: with one row
-            // block all 2*KS fragments are issued first; with two row blocks (each
-            // fragment feeds two MFMAs) a ring of two k-steps keeps registers low.
-            if constexpr (RB == 1) {
-                bf16x8 kf[KS][2];
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    kf[ks][0] = *(const bf16x8*)(kst + r32 * KSTR + ks * 16 + hf * 8);
-                    kf[ks][1] = *(const bf16x8*)(kst + (32 + r32) * KSTR + ks * 16 + hf * 8);
-                }
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    s[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][0], qf[0][ks], s[0][0], 0, 0, 0);
-                    s[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][1], qf[0][ks], s[0][1], 0, 0, 0);
-                }
-#if RELAXKV_ATTN_SCHED
-                __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // 4 LDS reads
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMAs
-                    if (ks + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-                }
-#endif
-            } else {
-                bf16x8 ka[2], kb[2];
-                ka[0] = *(const bf16x8*)(kst + r32 * KSTR + hf * 8);
-                ka[1] = *(const bf16x8*)(kst + (32 + r32) * KSTR + hf * 8);
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    if (ks + 1 < KS) {
-                        kb[0] = *(const bf16x8*)(kst + r32 * KSTR + (ks + 1) * 16 + hf * 8);
-                        kb[1] = *(const bf16x8*)(kst + (32 + r32) * KSTR + (ks + 1) * 16 + hf * 8);
-                    }
-#pragma unroll
-                    for (int rb = 0; rb < RB; ++rb) {
-                        s[rb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qf[rb][ks], s[rb][0], 0, 0, 0);
-                        s[rb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qf[rb][ks], s[rb][1], 0, 0, 0);
-                    }
-                    ka[0] = kb[0];
-                    ka[1] = kb[1];
-                }
+            for (int x = 0; x < 2 * KS; ++x) {
+                const bf16x8 cur = kf[x % KA];
+                if (x + KA < 2 * KS) kf[x % KA] = frag(x + KA);
+                s[x & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[x >> 1], s[x & 1], 0, 0, 0);
             }
+#if RELAXKV_ATTN_SCHED
+            __builtin_amdgcn_sched_group_barrier(0x100, KA, 0);
+#pragma unroll
+            for (int x = 0; x < 2 * KS; ++x) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                if (x + KA < 2 * KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+#endif
 #if RELAXKV_ATTN_SETPRIO
             __builtin_amdgcn_s_setprio(0);
 #endif
-            if (c0 + 63 > cmin) {                          // staircase step: mask
+        }
+        const int c0 = j * TK;
+        if (c0 + TK - 1 > cmin) {                      // staircase step: mask
+            const int ex = lim - c0 - 4 * hf;
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int key = c0 + 8 * (v >> 2) + 4 * hf + (v & 3);
-                        if (key > lim[rb]) s[rb][0][v] = -INFINITY;
-                        if (key + 32 > lim[rb]) s[rb][1][v] = -INFINITY;
-                    }
+            for (int v = 0; v < 16; ++v) {
+                if (8 * (v >> 2) + (v & 3) > ex) s[0][v] = -INFINITY;
+                if (32 + 8 * (v >> 2) + (v & 3) > ex) s[1][v] = -INFINITY;
             }
-            // Row max over the step in log2 units.  Lazy rescaling: the running
-            // max only moves when the step's max exceeds it by more than
-            // kRescaleSlack, so p <= 2^kRescaleSlack and most steps skip the O
-            // rescale.  Both halves of a row take the same decision.
-            float mx[RB];
-            bool need = false;
+        }
+        float m = fmaxf(s[0][0], s[1][0]);
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) {
-                float m = fmaxf(s[rb][0][0], s[rb][1][0]);
+        for (int v = 1; v < 16; ++v) m = fmaxf(m, fmaxf(s[0][v], s[1][v]));
+        const float mx = pair_max(m) * sl2;
+        const bool need = mx > m_run + kRescaleSlack;
+        if (__any(need)) {
+            const float m_new = need ? mx : m_run;
+            const float alpha = fast_exp2(m_run - m_new);
+            l_run *= alpha;
 #pragma unroll
-                for (int v = 1; v < 16; ++v) m = fmaxf(m, fmaxf(s[rb][0][v], s[rb][1][v]));
-                mx[rb] = pair_max(m) * sl2;
-                need |= mx[rb] > m_run[rb] + kRescaleSlack;
+            for (int db = 0; db < DB; ++db) o[db] *= alpha;
+            m_run = m_new;
+        }
+        bf16x8 pb[2][2];
+        float ls = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float p = fast_exp2(fmaf(s[kb][v], sl2, -m_run));
+                ls += p;
+                pb[kb][v >> 3][v & 7] = (__bf16)p;
             }
-            if (__any(need)) {
-#pragma unroll
-                for (int rb = 0; rb < RB; ++rb) {
-                    const float m_new = mx[rb] > m_run[rb] + kRescaleSlack ? mx[rb] : m_run[rb];
-                    const float alpha = fast_exp2(m_run[rb] - m_new);
-                    l_run[rb] *= alpha;
-#pragma unroll
-                    for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
-                    m_run[rb] = m_new;
-                }
-            }
-            // P^T as bf16 B operands: pb[rb][kb][k2] holds values 8*k2 .. 8*k2+7.
-            bf16x8 pb[RB][2][2];
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) {
-                float ls = 0.f;
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const float p = fast_exp2(fmaf(s[rb][kb][v], sl2, -m_run[rb]));
-                        ls += p;
-                        pb[rb][kb][v >> 3][v & 7] = (__bf16)p;
-                    }
-                l_run[rb] += ls;
-            }
-            // O^T += V^T P^T
+        l_run += ls;
+        // O^T += V^T P^T
+        {
+            int vb0 = v_base0, vb1 = v_base1;
+            asm volatile("" : "+v"(vb0), "+v"(vb1));
+            const char* vst = (const char*)Vt[j & 3];
 #if RELAXKV_ATTN_SETPRIO
             __builtin_amdgcn_s_setprio(2);
 #endif
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int db = 0; db < DB; ++db) {
+                for (int db = 0; db < DB; ++db)
 #pragma unroll
                     for (int k2 = 0; k2 < 2; ++k2) {
-                        const uint16_t* p0 = vst + vtr_off + (kb * 32 + k2 * 16) * VSTR + db * 32;
-                        const v4i16 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p0);
+                        const char* rowp = vst + (kb * 32 + k2 * 16) * ROWB;
+                        const v4i16 a0 =
+                            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(rowp + (vb0 ^ (db << 6))));
                         const v4i16 a1 =
-                            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 8 * VSTR));
-                        const bf16x8 vv = __builtin_bit_cast(
-                            bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-                        for (int rb = 0; rb < RB; ++rb)
-                            o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pb[rb][kb][k2],
-                                                                                o[rb][db], 0, 0, 0);
+                            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(rowp + (vb1 ^ (db << 6))));
+                        const bf16x8 vv =
+                            __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+                        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pb[kb][k2], o[db], 0, 0, 0);
                     }
-                }
-            }
 #if RELAXKV_ATTN_SETPRIO
             __builtin_amdgcn_s_setprio(0);
 #endif
         }
     }
 
+    const float l_tot = pair_sum(l_run);
+    if (!valid) return;
+    const bool empty = lim < 0;
+    const float inv = empty ? 0.f : 1.0f / l_tot;
+    uint16_t* out = (uint16_t*)a.out + ((size_t)t_row * a.H + head) * D;
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        const float l_tot = pair_sum(l_run[rb]);
-        if (!valid[rb]) continue;
-        const bool empty = lim[rb] < 0;
-        const float inv = empty ? 0.f : 1.0f / l_tot;
-        uint16_t* out = (uint16_t*)a.out + ((size_t)t_of[rb] * a.H + head_of[rb]) * D;
+    for (int db = 0; db < DB; ++db) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int d0 = db * 32 + 8 * j + 4 * hf;
-                const uint32_t lo = (uint32_t)f32_to_bf16_bits(o[rb][db][4 * j] * inv) |
-                                    ((uint32_t)f32_to_bf16_bits(o[rb][db][4 * j + 1] * inv) << 16);
-                const uint32_t hi = (uint32_t)f32_to_bf16_bits(o[rb][db][4 * j + 2] * inv) |
-                                    ((uint32_t)f32_to_bf16_bits(o[rb][db][4 * j + 3] * inv) << 16);
-                *(u32x2*)(out + d0) = u32x2{lo, hi};
-            }
+        for (int jj = 0; jj < 4; ++jj) {
+            const int d0 = db * 32 + 8 * jj + 4 * hf;
+            const uint32_t lo = (uint32_t)f32_to_bf16_bits(o[db][4 * jj] * inv) |
+                                ((uint32_t)f32_to_bf16_bits(o[db][4 * jj + 1] * inv) << 16);
+            const uint32_t hi = (uint32_t)f32_to_bf16_bits(o[db][4 * jj + 2] * inv) |
+                                ((uint32_t)f32_to_bf16_bits(o[db][4 * jj + 3] * inv) << 16);
+            *(u32x2*)(out + d0) = u32x2{lo, hi};
         }
-        if (a.lse && hf == 0)
-            a.lse[(size_t)t_of[rb] * a.H + head_of[rb]] =
-                empty ? -INFINITY : (m_run[rb] + __log2f(l_tot)) * kLn2;
     }
+    if (a.lse && hf == 0)
+        a.lse[(size_t)t_row * a.H + head] = empty ? -INFINITY : (m_run + __log2f(l_tot)) * kLn2;
 }
 
 // ----------------------------------------------------------------- fp32 VALU
@@ -447,16 +391,13 @@ __global__ __launch_bounds__(64) void attn_f32(AttnArgs a) {
 }
 
 constexpr int kNW = RELAXKV_ATTN_WAVES;
-constexpr int kBN = RELAXKV_ATTN_TILE;
-constexpr int kRB = RELAXKV_ATTN_ROWBLOCKS;
-static_assert(kAttnRows == kNW * kRB * 32, "rows per workgroup");
+static_assert(kAttnRows == kNW * 32, "rows per workgroup");
 
 template <int D, bool FULL>
 void launch_one(const AttnArgs& a, bool bf16, int n_bound, hipStream_t st) {
     if (bf16) {
         const int ntiles = (n_bound + a.BT - 1) / a.BT;
-        hipLaunchKernelGGL((attn_bf16<D, FULL, kNW, kBN, kRB>), dim3(ntiles * a.Hkv), dim3(kNW * 64),
-                           0, st, a);
+        hipLaunchKernelGGL((attn_bf16<D, FULL, kNW>), dim3(ntiles * a.Hkv), dim3(kNW * 64), 0, st, a);
     } else {
         hipLaunchKernelGGL((attn_f32<D, FULL>), dim3(n_bound, a.H), dim3(64), 0, st, a);
     }
@@ -494,7 +435,7 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.G = p.H / p.H_kv;
     a.T = p.T_c;
     a.layer = layer;
-    a.BT = bf16 ? kNW * kRB * 32 / a.G : 1;
+    a.BT = bf16 ? kAttnRows / a.G : 1;
     a.scale = p.softmax_scale > 0.f ? p.softmax_scale : 1.0f / sqrtf((float)p.d);
     // |R_l| <= |union of S_l' for l' >= l| <= min(T_c, (L - l) k) for RelaxKV's
     // targets, <= T_c for a global target list; the device count decides which

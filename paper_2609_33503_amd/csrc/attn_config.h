@@ -3,27 +3,20 @@
 
 namespace relaxkv {
 
-// Tile configuration of the bf16 MFMA attention kernel (compile-time; the
-// defaults are the tuned MI355X configuration).
+// Defaults are the tuned MI355X configuration.
 #ifndef RELAXKV_ATTN_WAVES
-#define RELAXKV_ATTN_WAVES 8        // waves per workgroup
+#define RELAXKV_ATTN_WAVES 12       // waves (32 rows each) per workgroup; one workgroup per CU
 #endif
-#ifndef RELAXKV_ATTN_TILE
-#define RELAXKV_ATTN_TILE 128       // keys per LDS tile (double-buffered)
+#ifndef RELAXKV_ATTN_KAHEAD
+#define RELAXKV_ATTN_KAHEAD 4       // K fragments read from LDS ahead of their MFMA
 #endif
 #ifndef RELAXKV_ATTN_SCHED
 #define RELAXKV_ATTN_SCHED 1        // interleave K-fragment LDS reads with the QK^T MFMAs
 #endif
 #ifndef RELAXKV_ATTN_SETPRIO
-#define RELAXKV_ATTN_SETPRIO 1      // raise wave priority during MFMA phases
-#endif
-#ifndef RELAXKV_ATTN_VPAD
-#define RELAXKV_ATTN_VPAD 32        // V tile row padding (elements): conflict-free transposing reads
-#endif
-#ifndef RELAXKV_ATTN_ROWBLOCKS
-#define RELAXKV_ATTN_ROWBLOCKS 1    // 32-row MFMA blocks per wave
+#define RELAXKV_ATTN_SETPRIO 0      // raise wave priority during MFMA phases
 #endif
 // (target, head) rows per workgroup: a GQA group of G heads must fit.
-constexpr int kAttnRows = RELAXKV_ATTN_WAVES * RELAXKV_ATTN_ROWBLOCKS * 32;
+constexpr int kAttnRows = RELAXKV_ATTN_WAVES * 32;
 
 }  // namespace relaxkv

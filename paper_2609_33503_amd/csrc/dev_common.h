@@ -118,4 +118,22 @@ __device__ __forceinline__ void wait_loads_barrier() {
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
+// The same fills written as inline assembly (M0 = the wave's LDS byte address,
+// lane l's bytes land at M0 + size * l).  The compiler does not see an LDS write
+// here, so it adds no vector-memory waits before later LDS reads: the caller
+// orders each fill and its readers with explicit s_waitcnt vmcnt counts and
+// barriers.  Waits the compiler inserts for its own loads stay correct, since
+// fills it does not count only make an in-order count wait longer.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(lds_void*)p;
+}
+__device__ __forceinline__ void fill_lds16(const void* src, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(src), "s"(lds) : "memory", "m0");
+}
+__device__ __forceinline__ void fill_lds4(const void* src, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+                 :: "v"(src), "s"(lds) : "memory", "m0");
+}
+
 }  // namespace relaxkv
