@@ -251,10 +251,21 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
                 if (32 + 8 * (v >> 2) + (v & 3) > ex) s[1][v] = -INFINITY;
             }
         }
+#if RELAXKV_ATTN_LEAN
+        // Two chains of 3-input maxima (two new values per instruction).
+        float m0 = fmaxf(s[0][0], s[0][1]), m1 = fmaxf(s[1][0], s[1][1]);
+#pragma unroll
+        for (int v = 2; v < 16; v += 2) {
+            m0 = fmaxf(fmaxf(m0, s[0][v]), s[0][v + 1]);
+            m1 = fmaxf(fmaxf(m1, s[1][v]), s[1][v + 1]);
+        }
+        const float mx = pair_max(fmaxf(m0, m1)) * sl2;
+#else
         float m = fmaxf(s[0][0], s[1][0]);
 #pragma unroll
         for (int v = 1; v < 16; ++v) m = fmaxf(m, fmaxf(s[0][v], s[1][v]));
         const float mx = pair_max(m) * sl2;
+#endif
         const bool need = mx > m_run + kRescaleSlack;
         if (__any(need)) {
             const float m_new = need ? mx : m_run;
@@ -265,6 +276,31 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
             m_run = m_new;
         }
         bf16x8 pb[2][2];
+#if RELAXKV_ATTN_LEAN
+        // The row sum adds the bf16 probabilities that the PV product uses, two
+        // per dot2 instruction, in four chains.
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                pb[kb][v >> 3][v & 7] = (__bf16)fast_exp2(fmaf(s[kb][v], sl2, -m_run));
+        {
+            typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+            const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+            float ls0 = 0.f, ls1 = 0.f, ls2 = 0.f, ls3 = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int k2 = 0; k2 < 2; ++k2) {
+                    const bf16x8 q8 = pb[kb][k2];
+                    ls0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(q8, q8, 0, 1), one2, ls0, false);
+                    ls1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(q8, q8, 2, 3), one2, ls1, false);
+                    ls2 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(q8, q8, 4, 5), one2, ls2, false);
+                    ls3 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(q8, q8, 6, 7), one2, ls3, false);
+                }
+            l_run += (ls0 + ls1) + (ls2 + ls3);
+        }
+#else
         float ls = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -275,6 +311,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
                 pb[kb][v >> 3][v & 7] = (__bf16)p;
             }
         l_run += ls;
+#endif
         // O^T += V^T P^T
         {
             int vb0 = v_base0, vb1 = v_base1;

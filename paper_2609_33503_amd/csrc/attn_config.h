@@ -16,6 +16,9 @@ namespace relaxkv {
 #ifndef RELAXKV_ATTN_SETPRIO
 #define RELAXKV_ATTN_SETPRIO 0      // raise wave priority during MFMA phases
 #endif
+#ifndef RELAXKV_ATTN_LEAN
+#define RELAXKV_ATTN_LEAN 1         // 3-input max chains and bf16 dot2 row sums in the softmax
+#endif
 // (target, head) rows per workgroup: a GQA group of G heads must fit.
 constexpr int kAttnRows = RELAXKV_ATTN_WAVES * 32;
 
