@@ -26,6 +26,7 @@ SMALL = {
     "llama-shape": synth.shrink(W["llama8b-8k"], L=3, T_c=1500),
     "qwen-shape": synth.shrink(W["qwen14b-16k"], L=3, T_c=2000),
     "qwen-planted": synth.shrink(W["qwen14b-32k-planted"], L=4, T_c=2600),
+    "qwen-latent": synth.shrink(W["qwen14b-32k-latent"], L=6, T_c=2600),
     "d64-bf16": synth.shrink(W["llama8b-8k"], L=2, T_c=777, H=8, H_kv=2, d=64, Qn=24),
     "mha-bf16": synth.shrink(W["llama8b-8k"], L=2, T_c=640, H=4, H_kv=4, Qn=8),
     "fp32-d128": synth.shrink(W["tiny-2L-1k-fp32"], L=2, T_c=300, d=128, H=6, H_kv=3, Qn=5),
@@ -64,7 +65,7 @@ def test_pipeline_small(gpu_lib, name):
     _pipeline(Case(SMALL[name]))
 
 
-@pytest.mark.parametrize("name", ["tiny", "qwen-planted"])
+@pytest.mark.parametrize("name", ["tiny", "qwen-planted", "qwen-latent"])
 def test_full_prefix_small(gpu_lib, name):
     _pipeline(Case(SMALL[name]), mode="full")
 
