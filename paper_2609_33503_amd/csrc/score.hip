@@ -24,6 +24,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 #include "dev_common.h"
 #include "internal.h"
 
@@ -31,45 +33,72 @@ namespace relaxkv {
 namespace {
 
 constexpr int kTileBytes = 16384;             // bytes of K per LDS tile (64 keys at d = 128)
-constexpr int kKeysPerSplit = 2048;           // keys per workgroup
-constexpr int kMaxWaves = 10;                 // row blocks per workgroup (one per wave)
-constexpr int kStages = 4;                    // LDS ring of K tiles
-constexpr int kRing = 4;                      // K fragments read ahead of their MFMA
+#ifndef RELAXKV_SCORE_SPLIT
+#define RELAXKV_SCORE_SPLIT 4096              // keys per workgroup
+#endif
+#ifndef RELAXKV_SCORE_KRING
+#define RELAXKV_SCORE_KRING 4                 // K fragments read ahead of their MFMA
+#endif
+constexpr int kKeysPerSplit = RELAXKV_SCORE_SPLIT;
+constexpr int kMaxWaves = 10;                 // 32-row query blocks per workgroup (one per wave)
+#ifndef RELAXKV_SCORE_STAGES
+#define RELAXKV_SCORE_STAGES 3                // LDS ring of K tiles
+#endif
+#ifndef RELAXKV_SCORE_WPE
+#define RELAXKV_SCORE_WPE 3                   // waves per SIMD the schedule is made for
+#endif
+constexpr int kStages = RELAXKV_SCORE_STAGES;
+constexpr int kRing = RELAXKV_SCORE_KRING;
+
+// Range a block's sum of exp2(s - m) may take before the statistics pass moves
+// its reference m (see score_pass_bf16).
+constexpr float kRefHi = 18446744073709551616.0f;     // 2^64
+constexpr float kRefLo = 5.42101086242752217e-20f;    // 2^-64
 
 template <int D>
 constexpr int tile_keys() { return kTileBytes / (2 * D); }
 
-// Two workgroups share a CU (LDS ~70 KB each), so the waves of one overlap the
-// barrier waits and vector phases of the other, and 2 x 10 waves spread evenly
-// over the 4 SIMDs.
-template <int NW>
-constexpr int score_waves_per_simd() { return (2 * NW + 3) / 4; }
+constexpr int pow2_ceil(int x) { return x <= 1 ? 1 : 2 * pow2_ceil((x + 1) / 2); }
 
 __host__ __device__ inline int round_up32(int x) { return (x + 31) / 32 * 32; }
 
-// The copy of a value held by the lane 32 away.  v_permlane32_swap with both
-// operands x returns, in each lane, x and its partner's x in its two results;
-// xor-ing both results with x leaves the partner's bits whichever result holds
-// which.
+// x plus the copy of x held by the lane 32 away (v_permlane32_swap with both
+// operands x returns x and the partner's x, in some order, in its two results).
+__device__ __forceinline__ float pair_add(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// The copy of x held by the lane 32 away (xor of both results with x leaves the
+// partner's bits whichever result holds which).
 __device__ __forceinline__ float pair_other(float x) {
     const uint32_t u = __float_as_uint(x);
     const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
     return __uint_as_float(r[0] ^ r[1] ^ u);
 }
 
-// One pass over the keys of a 2048-key split for the row set (l, g).  NW waves
-// each hold one 32-row block of the row set's queries in registers (row rho =
-// t*G + hh reads q[l][t][g*G + hh][:]); 16 KB tiles of K stream into a ring of
-// kStages swizzled LDS buffers by direct global->LDS loads, kStages-1 tiles
-// ahead of the MFMAs.
-//   STATS: S^T = K Q^T (one query row per lane): per-lane online (max, sum of
-//          exp2) over its keys, merged with the lane 32 away at the end ->
-//          stats[l][g][split][row] in log2 units.
-//   else:  S = Q K^T (one key per lane): per-lane sum of exp2(s - lse) over its
-//          16 rows, the two half-waves added, then a fixed-order sum over the
-//          waves in LDS -> part[l][g][key].
+// One pass over the keys of a split for the row set (l, g).  NW waves each hold
+// one 32-row block of the row set's queries in registers (row rho = t*G + hh
+// reads q[l][t][g*G + hh][:]); logits in log2 units are sl2 = scale * log2(e)
+// times the MFMA's dot products, applied in fp32.  16 KB tiles of K
+// stream into a ring of kStages swizzled LDS buffers by direct global->LDS
+// loads, kStages-1 tiles ahead of the MFMAs; the first NL/LPW waves issue LPW
+// loads per tile each, so one in-order count per wave says which tile has
+// landed.  Every logit costs one multiply, one exp2 and one add:
+//   STATS: S^T = K Q^T (one query row per lane, 16 keys per block): each lane
+//          sums exp2(s - m) over its keys against a reference m that starts at
+//          0 and moves to the block maximum only when a block's sum leaves
+//          [2^-64, 2^64] (the rescale keeps the sum exact; until some lane of
+//          the wave moves, m = 0 costs no subtraction); merged with the lane 32
+//          away -> stats[l][g][split][row] = (m, sum) in log2 units, i.e. the
+//          row's sum of exp2 over the split is sum * 2^m.
+//   else:  S = Q K^T - lse2 / sl2 (one key per lane, 16 rows per lane; the MFMA
+//          accumulator starts at -lse2 / sl2 of each row, its C operand): the
+//          lane sums exp2(sl2 * acc) over its rows, the two half-waves are
+//          added, then a fixed-order sum over the waves in LDS ->
+//          part[l][g][key].
 template <int D, int NW, bool STATS>
-__global__ __launch_bounds__(NW * 64, score_waves_per_simd<NW>()) void score_pass_bf16(
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV_SCORE_WPE, RELAXKV_SCORE_WPE))) void score_pass_bf16(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
     int Hkv, int G, int n_rows, int rows_pad, int n_split, float sl2,
     float2* __restrict__ stats, const float* __restrict__ lse2, const float* __restrict__ q_lse,
@@ -82,9 +111,12 @@ __global__ __launch_bounds__(NW * 64, score_waves_per_simd<NW>()) void score_pas
     constexpr int CH = D / 8;                       // 16-byte chunks per row
     constexpr int RPI = 64 / CH;                    // rows per wave-wide load
     constexpr int NL = TK / RPI;                    // wave-wide loads per tile (16)
-    constexpr int LPW = NL / NW;                    // loads per tile every wave issues (some one more)
-    constexpr int NI = (NL + NW - 1) / NW;
-    static_assert(LPW >= 1 && kStages == 4 && TK % 64 == 0, "pipeline shape");
+    constexpr int LPW = pow2_ceil((NL + NW - 1) / NW);   // loads per tile of a loading wave
+    constexpr int NLW = NL / LPW;                   // loading waves
+    constexpr int KA = kRing < KS ? kRing : KS;
+    static_assert(NL % LPW == 0 && NLW <= NW && kStages >= 2 && kStages <= 5 && TK % 64 == 0 &&
+                  NB % 2 == 0, "pipeline shape");
+    static_assert(RPI * ROWB == 1024, "one wave-wide load fills 1 KB");
     __shared__ __attribute__((aligned(1024))) uint16_t Ks[kStages][TK * D];
     __shared__ float colp[2][STATS ? 1 : NW][TK];
     __shared__ __attribute__((aligned(16))) float lrs[STATS ? 1 : NW][32];
@@ -95,39 +127,42 @@ __global__ __launch_bounds__(NW * 64, score_waves_per_simd<NW>()) void score_pas
     const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
     const int key0 = split * kKeysPerSplit;
     const int ntile = min(NT, (T - key0 + TK - 1) / TK);
+    const bool loader = w < NLW;
 
-    // Tile tt into stage tt % kStages.  Wave w issues loads j = w, w+NW, ...;
-    // lane l of load j fills (row j*RPI + l/CH, chunk l%CH).  Rows past T re-read
-    // row T-1: their logits are masked (STATS) or their sums never stored.
+    // Tile tt goes to stage tt % kStages.  Loading wave w issues loads
+    // j = w*LPW .. w*LPW + LPW-1; lane l of load j fills tile row j*RPI + l/CH at
+    // physical chunk l%CH, which holds logical chunk (l%CH) ^ swz(row).  Rows
+    // past T re-read row T-1: their logits are masked (STATS) or their sums
+    // never stored.
     const int lrow = lane / CH, pchunk = lane % CH;
-    uint32_t loff[NI];                              // byte offset of this lane's chunk in a tile
+    uint32_t loff[LPW];
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-        const int row = (w + i * NW) * RPI + lrow;
+    for (int i = 0; i < LPW; ++i) {
+        const int row = (w * LPW + i) * RPI + lrow;
         loff[i] = (uint32_t)(row * ROWB + ((pchunk ^ tile_swz<D>(row)) << 4));
     }
     auto issue_tile = [&](int tt) {
-        uint16_t* st = Ks[tt % kStages];
+        if (!loader) return;
+        const uint32_t st = lds_addr(Ks[tt % kStages]) + (uint32_t)(w * LPW) * 1024u;
         const int kb = key0 + tt * TK;
         const char* tb = (const char*)(Kg + (size_t)kb * D);
         const bool tail = kb + TK > T;
 #pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const int j = w + i * NW;
-            if (i < LPW || j < NL) {
-                uint32_t o = loff[i];
-                if (tail) {                                  // clamp the row to T-1
-                    const int row = j * RPI + lrow;
-                    o = (uint32_t)((min(kb + row, T - 1) - kb) * ROWB) + (o & (ROWB - 1));
-                }
-                load_lds16(tb + o, st + j * RPI * D);
+        for (int i = 0; i < LPW; ++i) {
+            uint32_t o = loff[i];
+            if (tail) {                                  // clamp the row to T-1
+                int row = (w * LPW + i) * RPI + lrow;
+                asm volatile("" : "+v"(row));
+                o = (uint32_t)(min(row, T - 1 - kb) * ROWB) + (o & (ROWB - 1));
             }
+            fill_lds16(tb + o, st + (uint32_t)i * 1024u);
         }
     };
     // Wait for tile tt (rem tiles were issued after it), then barrier.
     auto wait_tile = [&](int rem) {
-        if (rem >= 2) wait_loads_barrier<2 * LPW>();
-        else if (rem == 1) wait_loads_barrier<LPW>();
+        if (kStages >= 5 && rem >= 3) wait_loads_barrier<(kStages >= 5 ? 3 : 0) * LPW>();
+        else if (kStages >= 4 && rem >= 2) wait_loads_barrier<(kStages >= 4 ? 2 : 0) * LPW>();
+        else if (kStages >= 3 && rem >= 1) wait_loads_barrier<LPW>();
         else wait_loads_barrier<0>();
     };
     auto reduce_cols = [&](int tt, bool first_chunk) {   // colsum: fixed-order sum over waves
@@ -155,9 +190,12 @@ __global__ __launch_bounds__(NW * 64, score_waves_per_simd<NW>()) void score_pas
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) qf[ks] = bf16x8{};
         }
-        // Colsum: log2-sum-exp of the wave's 32 rows, kept in LDS (padding rows
-        // get +inf); the lane that accumulates rows 8j + 4hf + i reads
-        // lrs[w][8j + 4hf .. +3] as one 16-byte broadcast.
+        // Colsum: the C operand of the first MFMA of every block, -lse2 of the
+        // lane's rows 8j + 4hf + i (padding rows get -inf), staged through LDS
+        // (lane < 32 loads row w*32 + lane).
+        f32x16 cvec;
+        float m_ref = 0.f, z_run = 0.f;
+        bool moved = false;             // stats: some lane of the wave left reference 0
         if constexpr (!STATS) {
             if (lane < 32) {
                 const int row = rc0 + w * 32 + lane;
@@ -169,75 +207,116 @@ __global__ __launch_bounds__(NW * 64, score_waves_per_simd<NW>()) void score_pas
                 lrs[w][lane] = x;
             }
         }
-        float m_run = -INFINITY, z_run = 0.f;
 
-        __syncthreads();                                // LDS free from the previous row chunk
+        __syncthreads();          // Q and LSE loads done; LDS free from the previous row chunk
+        if constexpr (!STATS) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const f32x4 lr = *(const f32x4*)&lrs[w][8 * j + 4 * hf];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) cvec[4 * j + i] = -lr[i] / sl2;
+            }
+        }
+
+        // KS MFMAs of block (tt, b) into acc, K fragments read KA ahead.
+        auto mfma_block = [&](int tt, int b, f32x16& acc) {
+            int kbo = k_base;
+            asm volatile("" : "+v"(kbo));
+            const char* kp = (const char*)Ks[tt % kStages] + b * 32 * ROWB;
+            bf16x8 kf[KA];
+#pragma unroll
+            for (int i = 0; i < KA; ++i) kf[i] = *(const bf16x8*)(kp + (kbo ^ (i << 5)));
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 cur = kf[ks % KA];
+                if (ks + KA < KS) kf[ks % KA] = *(const bf16x8*)(kp + (kbo ^ ((ks + KA) << 5)));
+                const f32x16 c = ks > 0 ? acc : STATS ? f32x16{} : cvec;
+                if constexpr (STATS)
+                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[ks], c, 0, 0, 0);
+                else
+                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], cur, c, 0, 0, 0);
+            }
+        };
+        // Sum of exp2(sl2 * acc) over a block (minus m_ref when SUB).
+        auto exp_sum = [&](const f32x16& acc, auto sub) {
+            float z0 = 0.f, z1 = 0.f;
+#pragma unroll
+            for (int v = 0; v < 16; v += 2) {
+                if constexpr (decltype(sub)::value) {
+                    z0 += fast_exp2(fmaf(acc[v], sl2, -m_ref));
+                    z1 += fast_exp2(fmaf(acc[v + 1], sl2, -m_ref));
+                } else {
+                    z0 += fast_exp2(acc[v] * sl2);
+                    z1 += fast_exp2(acc[v + 1] * sl2);
+                }
+            }
+            return z0 + z1;
+        };
+        // Stats, block key base kb0: mask keys past T (acc[v] is key
+        // kb0 + 8(v/4) + 4hf + v%4 of row rho).
+        auto mask_tail = [&](int kb0, f32x16& acc) {
+            if (kb0 + 32 > T) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    if (kb0 + 8 * (v >> 2) + 4 * hf + (v & 3) >= T) acc[v] = -INFINITY;
+            }
+        };
+        // The vector work of block (tt, b) held in acc.  Stats: fold the block's
+        // sum into the row's running sum, moving the reference when the block's
+        // sum leaves [2^-64, 2^64] (rare).  Colsum: the block's column sums go to
+        // colp (both half-waves hold the same sum and store it to the same word,
+        // so no lane mask is needed).
+        auto consume = [&](int tt, int b, f32x16& acc) {
+            if constexpr (STATS) {
+                mask_tail(key0 + tt * TK + 32 * b, acc);
+                float zb = moved ? exp_sum(acc, std::true_type{}) : exp_sum(acc, std::false_type{});
+                const bool out = !(zb <= kRefHi) || z_run + zb < kRefLo;
+                if (__builtin_expect(out, 0)) {
+                    // New reference: the larger of the block maximum and the
+                    // log2 of what the row has summed so far, so neither the
+                    // block's terms nor the running sum exceed 16 times it.
+                    float mt = acc[0];
+#pragma unroll
+                    for (int v = 1; v < 16; ++v) mt = fmaxf(mt, acc[v]);
+                    mt *= sl2;
+                    const float lz = z_run > 0.f ? m_ref + __log2f(z_run) : -INFINITY;
+                    mt = fmaxf(mt, lz);
+                    if (mt > -INFINITY) {
+                        zb = 0.f;
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) zb += fast_exp2(fmaf(acc[v], sl2, -mt));
+                        z_run = fast_exp2(lz - mt);          // the running sum rescaled (<= 1)
+                        m_ref = mt;
+                    }
+                }
+                moved = moved || __any(out);
+                z_run += zb;
+            } else {
+                colp[tt & 1][STATS ? 0 : w][32 * b + r32] = pair_add(exp_sum(acc, std::false_type{}));
+            }
+        };
+
+        f32x16 acc[NB];
 #pragma unroll
         for (int tt = 0; tt < kStages - 1; ++tt)
             if (tt < ntile) issue_tile(tt);
         for (int tt = 0; tt < ntile; ++tt) {
+            // Tile tt has landed and every wave is past tile tt-1 (whose stage
+            // the next fill reuses and whose column sums are complete).
             wait_tile(min(kStages - 2, ntile - 1 - tt));
-            if (!STATS && tt > 0) reduce_cols(tt - 1, rc0 == 0);
+            if (!STATS && tt >= 1) reduce_cols(tt - 1, rc0 == 0);
             if (tt + kStages - 1 < ntile) issue_tile(tt + kStages - 1);
-            const char* kt = (const char*)Ks[tt % kStages];
-            const int kbase = key0 + tt * TK;
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
-                // 32-key block: KS MFMAs, K fragments read kRing ahead.
-                const char* kp = kt + b * 32 * ROWB;
-                bf16x8 kf[kRing];
-#pragma unroll
-                for (int i = 0; i < kRing; ++i) kf[i] = *(const bf16x8*)(kp + (k_base ^ (i << 5)));
-                f32x16 acc = f32x16{};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const bf16x8 cur = kf[ks % kRing];
-                    if (ks + kRing < KS) kf[ks % kRing] = *(const bf16x8*)(kp + (k_base ^ ((ks + kRing) << 5)));
-                    if constexpr (STATS)
-                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[ks], acc, 0, 0, 0);
-                    else
-                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], cur, acc, 0, 0, 0);
-                }
-                const int kb0 = kbase + 32 * b;
-                if constexpr (STATS) {
-                    // acc[v] = S[row r32][key kb0 + 8(v/4) + 4hf + v%4]
-                    if (kb0 + 32 > T) {
-#pragma unroll
-                        for (int v = 0; v < 16; ++v)
-                            if (kb0 + 8 * (v >> 2) + 4 * hf + (v & 3) >= T) acc[v] = -INFINITY;
-                    }
-                    float mt = acc[0];
-#pragma unroll
-                    for (int v = 1; v < 16; ++v) mt = fmaxf(mt, acc[v]);
-                    const float m_new = fmaxf(m_run, mt * sl2);
-                    const float mref = m_new == -INFINITY ? 0.f : m_new;
-                    float z = z_run * fast_exp2(m_run - mref);
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) z += fast_exp2(fmaf(acc[v], sl2, -mref));
-                    z_run = z;
-                    m_run = m_new;
-                } else {
-                    // acc[v] = S[row rc0 + w*32 + 8(v/4) + 4hf + v%4][key kb0 + r32]
-                    float cs = 0.f;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const f32x4 lr = *(const f32x4*)&lrs[w][8 * j + 4 * hf];
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) cs += fast_exp2(fmaf(acc[4 * j + i], sl2, -lr[i]));
-                    }
-                    const float other = pair_other(cs);
-                    if (hf == 0) colp[tt & 1][w][32 * b + r32] = cs + other;
-                }
+                mfma_block(tt, b, acc[b]);
+                consume(tt, b, acc[b]);
             }
         }
         if constexpr (STATS) {
             // merge with the lane 32 away (same row, the other half of the keys)
-            const float m2 = pair_other(m_run), z2 = pair_other(z_run);
-            const float M = fmaxf(m_run, m2);
-            float Z = 0.f;
-            if (M != -INFINITY)
-                Z = (m_run == -INFINITY ? 0.f : z_run * fast_exp2(m_run - M)) +
-                    (m2 == -INFINITY ? 0.f : z2 * fast_exp2(m2 - M));
+            const float m2 = pair_other(m_ref), z2 = pair_other(z_run);
+            const float M = fmaxf(m_ref, m2);
+            const float Z = z_run * fast_exp2(m_ref - M) + z2 * fast_exp2(m2 - M);
             if (hf == 0 && rho < rows_pad)
                 stats[(((size_t)l * Hkv + g) * n_split + split) * rows_pad + rho] = make_float2(M, Z);
         } else {
@@ -247,6 +326,7 @@ __global__ __launch_bounds__(NW * 64, score_waves_per_simd<NW>()) void score_pas
     }
 }
 
+// Per row: merge the splits' (m, sum) pairs into a log2-sum-exp.
 __global__ void score_merge(const float2* __restrict__ stats, int n_groups, int n_split,
                             int rows_pad, int n_rows, float* __restrict__ lse2) {
     const long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
@@ -263,7 +343,7 @@ __global__ void score_merge(const float2* __restrict__ stats, int n_groups, int 
     float Z = 0.f;
     for (int j = 0; j < n_split; ++j) {
         const float2 v = s[(size_t)j * rows_pad];
-        if (v.x != -INFINITY) Z += v.y * fast_exp2(v.x - M);
+        Z += v.y * fast_exp2(v.x - M);
     }
     lse2[i] = M + __log2f(Z);
 }
@@ -445,16 +525,17 @@ void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char*
     float* part = (float*)(ws + w.part_off);
     float* lse2 = (float*)(ws + w.lse_off);
     float2* stats = (float2*)(ws + w.stats_off);
+    const dim3 block(NW * 64);
     const dim3 grid(w.n_split, p.H_kv, p.L);
     if (!p.q_lse) {
-        hipLaunchKernelGGL((score_pass_bf16<D, NW, true>), grid, dim3(NW * 64), 0, st, q, kc,
-                           p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2,
-                           stats, (const float*)nullptr, (const float*)nullptr, part);
+        hipLaunchKernelGGL((score_pass_bf16<D, NW, true>), grid, block, 0, st, q, kc, p.T_c,
+                           p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2, stats,
+                           (const float*)nullptr, (const float*)nullptr, part);
         const long n = (long)p.L * p.H_kv * w.rows_pad;
         hipLaunchKernelGGL(score_merge, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                            (const float2*)stats, p.L * p.H_kv, w.n_split, w.rows_pad, n_rows, lse2);
     }
-    hipLaunchKernelGGL((score_pass_bf16<D, NW, false>), grid, dim3(NW * 64), 0, st, q, kc, p.T_c,
+    hipLaunchKernelGGL((score_pass_bf16<D, NW, false>), grid, block, 0, st, q, kc, p.T_c,
                        p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2, stats,
                        (const float*)lse2, p.q_lse, part);
 }
@@ -464,10 +545,10 @@ hipError_t launch_score_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, 
                              float* scores, hipStream_t st, float scale) {
     const float sl2 = scale * kLog2e;
     // One wave per 32-row block of the row set, up to kMaxWaves; larger row sets
-    // loop over row chunks of 8 blocks.
+    // loop over row chunks of kMaxWaves blocks.
     const int nrb = w.rows_pad / 32;
     if (nrb <= 4) launch_passes_bf16<D, 4>(p, w, ws, st, sl2);
-    else if (nrb <= 8 || nrb > kMaxWaves) launch_passes_bf16<D, 8>(p, w, ws, st, sl2);
+    else if (nrb <= 8) launch_passes_bf16<D, 8>(p, w, ws, st, sl2);
     else launch_passes_bf16<D, kMaxWaves>(p, w, ws, st, sl2);
     launch_finalize(p, w, ws, scores, st);
     return hipGetLastError();

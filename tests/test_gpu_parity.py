@@ -104,6 +104,29 @@ def test_supplied_lse_scoring(gpu_lib):
     assert_close(a_gpu, a_ref, w, "scores with supplied lse")
 
 
+@pytest.mark.parametrize("kind", ["large", "negative"])
+def test_scores_extreme_logits(gpu_lib, kind):
+    """Logits far outside the unit range (tens to hundreds of log2 units): the
+    row statistics must stay exact when a block's sum of exp2 would overflow
+    fp32 ("large": spread of about +-150 log2 units) or underflow against the
+    starting reference ("negative": every logit near -500 log2 units)."""
+    w = synth.shrink(W["llama8b-8k"], L=2, T_c=1500, Qn=4)
+    case = Case(w)
+    g = torch.Generator().manual_seed(7)
+    if kind == "large":
+        case.kc.mul_(4000.0)
+    else:
+        u = torch.randn(w.d, generator=g, dtype=torch.float64)
+        u /= u.norm()
+        noise = torch.randn(w.L, w.H_kv, w.T_c, w.d, generator=g, dtype=torch.float64) * 40.0
+        case.q.copy_(u.expand_as(case.q).to(case.q.dtype))
+        case.kc.copy_((-3925.0 * u + noise).to(case.kc.dtype))
+    a_gpu = case.gpu_scores().cpu().numpy()
+    a_ref, _, lse_ref = case.oracle_scores()
+    assert np.abs(lse_ref).max() > 60.0          # the logits are in the extreme range
+    assert_close(a_gpu, a_ref, w, f"scores ({kind} logits)")
+
+
 def test_equal_keys_select_first_k(gpu_lib):
     w = synth.shrink(W["llama8b-8k"], L=2, T_c=700, Qn=4)
     case = Case(w)
