@@ -30,6 +30,11 @@ SMALL = {
     "d64-bf16": synth.shrink(W["llama8b-8k"], L=2, T_c=777, H=8, H_kv=2, d=64, Qn=24),
     "mha-bf16": synth.shrink(W["llama8b-8k"], L=2, T_c=640, H=4, H_kv=4, Qn=8),
     "fp32-d128": synth.shrink(W["tiny-2L-1k-fp32"], L=2, T_c=300, d=128, H=6, H_kv=3, Qn=5),
+    # 100 query tokens x 5 heads = 500 score rows: the scoring passes take two
+    # row chunks per workgroup (the column sums accumulate across chunks)
+    "long-query": synth.shrink(W["qwen14b-16k"], L=2, T_c=1300, Qn=100),
+    "gqa16": synth.shrink(W["llama8b-8k"], L=2, T_c=900, H=32, H_kv=2, Qn=8),
+    "gqa12-d64": synth.shrink(W["llama8b-8k"], L=3, T_c=1100, H=24, H_kv=2, d=64, Qn=12),
 }
 
 
