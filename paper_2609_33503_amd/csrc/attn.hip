@@ -104,6 +104,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     constexpr int NL = TK / RPI;           // wave-wide loads per step and tensor
     constexpr int PPW = (NL + NW - 1) / NW;   // K/V load pairs of the busiest wave
     constexpr int NWAIT = 2 * PPW;         // its fills per step
+    constexpr int NWAIT_TAIL = 2 * (NL / NW);  // fills per step of the least busy wave
     __shared__ __attribute__((aligned(1024))) uint16_t Kt[NST][TK * D];
     __shared__ __attribute__((aligned(1024))) uint16_t Vt[NST][TK * D];
     __shared__ __attribute__((aligned(256))) int32_t Ix[NST][2][TK];   // [U or rank, src]
@@ -202,8 +203,14 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     for (int j = 0; j < S; ++j) {
         // The fills of step j and the indices of step j+3 are complete (only the
         // fills of step j+2 may be in flight), and every wave is done with step
-        // j-1, whose buffers the fills of step j+3 reuse.
-        wait_loads_barrier<NWAIT>();
+        // j-1, whose buffers the fills of step j+3 reuse.  Loads complete in
+        // order, so a wave's fills of step j are done once at most as many of
+        // its loads are outstanding as it issued after them: the fills of steps
+        // j+1 and j+2 (at least NWAIT loads while both steps exist), only those
+        // of step j+1 near the end (at least NWAIT_TAIL), none in the last step.
+        if (j + 2 < S) wait_loads_barrier<NWAIT>();
+        else if (j + 1 < S) wait_loads_barrier<NWAIT_TAIL>();
+        else wait_loads_barrier<0>();
         if (j + NST < S) issue_idx(j + NST);
         if (j + NST - 1 < S) issue_rows(j + NST - 1);
         // S^T = K Q^T: s[kb][v] = S[row][key 64 j + 32 kb + 8(v/4) + 4 hf + v%4]
