@@ -2,19 +2,20 @@
 //   A_l[h,t,i] = softmax_i(sigma <q_{l,t,h}, k_{l,g(h),i}>),
 //   p_{l,i} = (1/(H Qn)) sum_{h,t} A_l[h,t,i],   a_{l,i} = MinMax_i(p_{l,i}).
 //
-// bf16 path (bf16 MFMA, fp32 accumulation), per layer l and KV head g the
-// Qn*G query rows that share g form one row set; each workgroup takes a split
-// of 2048 contiguous keys, each wave holds one 32-row block of the row set's
-// queries in registers, and 16 KB tiles of K stream through a 4-deep ring of
-// LDS buffers filled by direct global->LDS loads (two workgroups per CU):
-//   1. score_pass<STATS> -- S^T = K Q^T (one query row per lane) and each
-//      row's (max, sum of exp2) over the split.          [skipped with q_lse]
+// bf16 path (bf16 MFMA, fp32 accumulation).  Per layer l and KV head g the
+// Qn*G query rows that share g form one row set; workgroups take splits of
+// 4096 contiguous keys:
+//   1. score_stats_bf16 -- each wave holds one 32-row block of the row set's
+//      queries in registers while 16 KB tiles of K stream through a ring of
+//      LDS buffers (direct global->LDS loads); S^T = K Q^T (one query row per
+//      lane) gives each row's (max, sum of exp2) over the split.
+//                                                        [skipped with q_lse]
 //   2. score_merge  -- per row, merge the splits into a log2-sum-exp.
-//   3. score_pass<colsum> -- the same tiles as S = Q K^T (one key per lane):
-//      every lane sums exp2(s - lse) over its rows, the waves' partial sums are
-//      added in a fixed order, giving the pooled mass of each key for this KV
-//      head.  K is read once more (from the last-level cache when the layer's
-//      K fits there).
+//   3. score_colsum_kreg -- the row set is staged once into LDS with each
+//      row's -lse as an extra k-step; each wave loads its own keys from HBM
+//      straight into registers and runs every row block against them
+//      (S = Q K^T - lse, one key per lane), summing exp2 over the rows: the
+//      pooled mass of each key for this KV head.
 //   4. score_pool / score_minmax -- the fixed-order sum over KV heads and the
 //      1/(H Qn) factor with per-block extrema, then the MinMax normalisation.
 // float32 path: plain VALU kernels with the same four steps (used for fp32
@@ -48,10 +49,17 @@ constexpr int kMaxWaves = 10;                 // 32-row query blocks per workgro
 #define RELAXKV_SCORE_WPE 3                   // waves per SIMD the schedule is made for
 #endif
 constexpr int kStages = RELAXKV_SCORE_STAGES;
+#ifndef RELAXKV_SCORE_KREG_NW
+#define RELAXKV_SCORE_KREG_NW 8               // waves per workgroup of that pass
+#endif
+#ifndef RELAXKV_SCORE_KREG_NKB
+#define RELAXKV_SCORE_KREG_NKB 2              // 32-key blocks per wave and round
+#endif
+constexpr int kKregRowBlocks = 10;            // 32-row blocks staged per row chunk
 constexpr int kRing = RELAXKV_SCORE_KRING;
 
 // Range a block's sum of exp2(s - m) may take before the statistics pass moves
-// its reference m (see score_pass_bf16).
+// its reference m (see score_stats_bf16).
 constexpr float kRefHi = 18446744073709551616.0f;     // 2^64
 constexpr float kRefLo = 5.42101086242752217e-20f;    // 2^-64
 
@@ -77,32 +85,26 @@ __device__ __forceinline__ float pair_other(float x) {
     return __uint_as_float(r[0] ^ r[1] ^ u);
 }
 
-// One pass over the keys of a split for the row set (l, g).  NW waves each hold
-// one 32-row block of the row set's queries in registers (row rho = t*G + hh
-// reads q[l][t][g*G + hh][:]); logits in log2 units are sl2 = scale * log2(e)
-// times the MFMA's dot products, applied in fp32.  16 KB tiles of K
-// stream into a ring of kStages swizzled LDS buffers by direct global->LDS
-// loads, kStages-1 tiles ahead of the MFMAs; the first NL/LPW waves issue LPW
-// loads per tile each, so one in-order count per wave says which tile has
-// landed.  Every logit costs one multiply, one exp2 and one add:
-//   STATS: S^T = K Q^T (one query row per lane, 16 keys per block): each lane
-//          sums exp2(s - m) over its keys against a reference m that starts at
-//          0 and moves to the block maximum only when a block's sum leaves
-//          [2^-64, 2^64] (the rescale keeps the sum exact; until some lane of
-//          the wave moves, m = 0 costs no subtraction); merged with the lane 32
-//          away -> stats[l][g][split][row] = (m, sum) in log2 units, i.e. the
-//          row's sum of exp2 over the split is sum * 2^m.
-//   else:  S = Q K^T - lse2 / sl2 (one key per lane, 16 rows per lane; the MFMA
-//          accumulator starts at -lse2 / sl2 of each row, its C operand): the
-//          lane sums exp2(sl2 * acc) over its rows, the two half-waves are
-//          added, then a fixed-order sum over the waves in LDS ->
-//          part[l][g][key].
-template <int D, int NW, bool STATS>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV_SCORE_WPE, RELAXKV_SCORE_WPE))) void score_pass_bf16(
+// Row statistics over the keys of a split for the row set (l, g).  NW waves
+// each hold one 32-row block of the row set's queries in registers (row
+// rho = t*G + hh reads q[l][t][g*G + hh][:]); logits in log2 units are
+// sl2 = scale * log2(e) times the MFMA's dot products, applied in fp32.  16 KB
+// tiles of K stream into a ring of kStages swizzled LDS buffers by direct
+// global->LDS loads, kStages-1 tiles ahead of the MFMAs; the first NL/LPW waves
+// issue LPW loads per tile each, so one in-order count per wave says which tile
+// has landed.  S^T = K Q^T (one query row per lane, 16 keys per block): each
+// lane sums exp2(s - m) over its keys against a reference m that starts at 0
+// and moves to the block maximum only when a block's sum leaves [2^-64, 2^64]
+// (the rescale keeps the sum exact; until some lane of the wave moves, m = 0
+// costs no subtraction); merged with the lane 32 away ->
+// stats[l][g][split][row] = (m, sum) in log2 units, i.e. the row's sum of exp2
+// over the split is sum * 2^m.  Every logit costs one multiply, one exp2 and
+// one add.
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV_SCORE_WPE, RELAXKV_SCORE_WPE))) void score_stats_bf16(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
     int Hkv, int G, int n_rows, int rows_pad, int n_split, float sl2,
-    float2* __restrict__ stats, const float* __restrict__ lse2, const float* __restrict__ q_lse,
-    float* __restrict__ part) {
+    float2* __restrict__ stats) {
     constexpr int TK = tile_keys<D>();              // keys per tile
     constexpr int NT = kKeysPerSplit / TK;          // tiles per split
     constexpr int KS = D / 16;
@@ -118,8 +120,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
                   NB % 2 == 0, "pipeline shape");
     static_assert(RPI * ROWB == 1024, "one wave-wide load fills 1 KB");
     __shared__ __attribute__((aligned(1024))) uint16_t Ks[kStages][TK * D];
-    __shared__ float colp[2][STATS ? 1 : NW][TK];
-    __shared__ __attribute__((aligned(16))) float lrs[STATS ? 1 : NW][32];
 
     const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, hf = lane >> 5;
@@ -132,8 +132,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
     // Tile tt goes to stage tt % kStages.  Loading wave w issues loads
     // j = w*LPW .. w*LPW + LPW-1; lane l of load j fills tile row j*RPI + l/CH at
     // physical chunk l%CH, which holds logical chunk (l%CH) ^ swz(row).  Rows
-    // past T re-read row T-1: their logits are masked (STATS) or their sums
-    // never stored.
+    // past T re-read row T-1; their logits are masked.
     const int lrow = lane / CH, pchunk = lane % CH;
     uint32_t loff[LPW];
 #pragma unroll
@@ -165,16 +164,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
         else if (kStages >= 3 && rem >= 1) wait_loads_barrier<LPW>();
         else wait_loads_barrier<0>();
     };
-    auto reduce_cols = [&](int tt, bool first_chunk) {   // colsum: fixed-order sum over waves
-        const int key = key0 + tt * TK + tid;
-        if (tid < TK && key < T) {
-            float v = 0.f;
-#pragma unroll
-            for (int ww = 0; ww < NW; ++ww) v += colp[tt & 1][STATS ? 0 : ww][tid];
-            float* dst = part + ((size_t)l * Hkv + g) * T + key;
-            *dst = first_chunk ? v : *dst + v;
-        }
-    };
     // K fragment (tile row 32b + r32, logical chunk 2ks + hf) byte offset.
     const int k_base = r32 * ROWB | ((hf ^ tile_swz<D>(r32)) << 4);
 
@@ -190,33 +179,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) qf[ks] = bf16x8{};
         }
-        // Colsum: the C operand of the first MFMA of every block, -lse2 of the
-        // lane's rows 8j + 4hf + i (padding rows get -inf), staged through LDS
-        // (lane < 32 loads row w*32 + lane).
-        f32x16 cvec;
         float m_ref = 0.f, z_run = 0.f;
-        bool moved = false;             // stats: some lane of the wave left reference 0
-        if constexpr (!STATS) {
-            if (lane < 32) {
-                const int row = rc0 + w * 32 + lane;
-                float x = INFINITY;
-                if (row < n_rows) {
-                    x = q_lse ? q_lse[((size_t)l * Qn + row / G) * H + g * G + row % G] * kLog2e
-                              : lse2[((size_t)l * Hkv + g) * rows_pad + row];
-                }
-                lrs[w][lane] = x;
-            }
-        }
-
-        __syncthreads();          // Q and LSE loads done; LDS free from the previous row chunk
-        if constexpr (!STATS) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const f32x4 lr = *(const f32x4*)&lrs[w][8 * j + 4 * hf];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) cvec[4 * j + i] = -lr[i] / sl2;
-            }
-        }
+        bool moved = false;             // some lane of the wave left reference 0
+        __syncthreads();                // LDS free from the previous row chunk
 
         // KS MFMAs of block (tt, b) into acc, K fragments read KA ahead.
         auto mfma_block = [&](int tt, int b, f32x16& acc) {
@@ -230,11 +195,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
             for (int ks = 0; ks < KS; ++ks) {
                 const bf16x8 cur = kf[ks % KA];
                 if (ks + KA < KS) kf[ks % KA] = *(const bf16x8*)(kp + (kbo ^ ((ks + KA) << 5)));
-                const f32x16 c = ks > 0 ? acc : STATS ? f32x16{} : cvec;
-                if constexpr (STATS)
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[ks], c, 0, 0, 0);
-                else
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], cur, c, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[ks], ks > 0 ? acc : f32x16{},
+                                                              0, 0, 0);
             }
         };
         // Sum of exp2(sl2 * acc) over a block (minus m_ref when SUB).
@@ -252,7 +214,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
             }
             return z0 + z1;
         };
-        // Stats, block key base kb0: mask keys past T (acc[v] is key
+        // Block key base kb0: mask keys past T (acc[v] is key
         // kb0 + 8(v/4) + 4hf + v%4 of row rho).
         auto mask_tail = [&](int kb0, f32x16& acc) {
             if (kb0 + 32 > T) {
@@ -261,13 +223,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
                     if (kb0 + 8 * (v >> 2) + 4 * hf + (v & 3) >= T) acc[v] = -INFINITY;
             }
         };
-        // The vector work of block (tt, b) held in acc.  Stats: fold the block's
-        // sum into the row's running sum, moving the reference when the block's
-        // sum leaves [2^-64, 2^64] (rare).  Colsum: the block's column sums go to
-        // colp (both half-waves hold the same sum and store it to the same word,
-        // so no lane mask is needed).
+        // The vector work of block (tt, b) held in acc: fold the block's sum
+        // into the row's running sum, moving the reference when the block's sum
+        // leaves [2^-64, 2^64] (rare).
         auto consume = [&](int tt, int b, f32x16& acc) {
-            if constexpr (STATS) {
+            {
                 mask_tail(key0 + tt * TK + 32 * b, acc);
                 float zb = moved ? exp_sum(acc, std::true_type{}) : exp_sum(acc, std::false_type{});
                 const bool out = !(zb <= kRefHi) || z_run + zb < kRefLo;
@@ -291,8 +251,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
                 }
                 moved = moved || __any(out);
                 z_run += zb;
-            } else {
-                colp[tt & 1][STATS ? 0 : w][32 * b + r32] = pair_add(exp_sum(acc, std::false_type{}));
             }
         };
 
@@ -302,9 +260,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
             if (tt < ntile) issue_tile(tt);
         for (int tt = 0; tt < ntile; ++tt) {
             // Tile tt has landed and every wave is past tile tt-1 (whose stage
-            // the next fill reuses and whose column sums are complete).
+            // the next fill reuses).
             wait_tile(min(kStages - 2, ntile - 1 - tt));
-            if (!STATS && tt >= 1) reduce_cols(tt - 1, rc0 == 0);
             if (tt + kStages - 1 < ntile) issue_tile(tt + kStages - 1);
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
@@ -312,17 +269,136 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV
                 consume(tt, b, acc[b]);
             }
         }
-        if constexpr (STATS) {
-            // merge with the lane 32 away (same row, the other half of the keys)
-            const float m2 = pair_other(m_ref), z2 = pair_other(z_run);
-            const float M = fmaxf(m_ref, m2);
-            const float Z = z_run * fast_exp2(m_ref - M) + z2 * fast_exp2(m2 - M);
-            if (hf == 0 && rho < rows_pad)
-                stats[(((size_t)l * Hkv + g) * n_split + split) * rows_pad + rho] = make_float2(M, Z);
-        } else {
-            __syncthreads();
-            reduce_cols(ntile - 1, rc0 == 0);
+        // merge with the lane 32 away (same row, the other half of the keys)
+        const float m2 = pair_other(m_ref), z2 = pair_other(z_run);
+        const float M = fmaxf(m_ref, m2);
+        const float Z = z_run * fast_exp2(m_ref - M) + z2 * fast_exp2(m2 - M);
+        if (hf == 0 && rho < rows_pad)
+            stats[(((size_t)l * Hkv + g) * n_split + split) * rows_pad + rho] = make_float2(M, Z);
+    }
+}
+
+// Column-sum pass with the keys in registers (rows known by their log2-sum-exp).
+// A workgroup takes one (layer l, KV head g, key split).  The query rows of the
+// group are staged once into LDS, fragment-major: fragment (rb, j) is the MFMA A
+// operand of 32-row block rb and k-step j, lane l's 16 bytes at 16 l, so every
+// read is one conflict-free ds_read_b128 at a fixed offset from the lane's base.
+// The last k-step carries the row's -lse2 / sl2 as three bf16 terms (their sum
+// is the fp32 value exactly) against a constant B fragment of ones, so the
+// accumulator ends at s - lse2 / sl2 and exp2(sl2 * acc) is the probability.
+// Each wave owns NKB blocks of 32 keys per round, loads them from HBM straight
+// into registers (the B operand of S = Q K^T: lane l holds key l % 32, the
+// 16-byte chunk 2j + l / 32 of k-step j) and runs every row block against them,
+// so a query fragment read from LDS feeds NKB MFMAs and K needs no LDS at all.
+// Per lane the 16 rows of a block are summed in fp32 in a fixed order, then the
+// two half-waves are added: part[l][g][key] (added to the earlier row chunks'
+// sum when the row set takes several chunks).  The next round's keys are
+// loaded while the last row block's exp2 work runs.  Waves never wait for one
+// another inside a row chunk.
+template <int D, int NW, int NKB>
+__global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
+    int Hkv, int G, int n_rows, int rows_pad, int keys_per_split, float sl2,
+    const float* __restrict__ lse2, const float* __restrict__ q_lse, float* __restrict__ part) {
+    constexpr int KS = D / 16;                      // k-steps of the dot product
+    constexpr int KF = KS + 1;                      // plus the -lse2 / sl2 step
+    constexpr int NRB = kKregRowBlocks;             // row blocks per chunk
+    constexpr int KPW = NKB * 32;                   // keys of a wave per round
+    constexpr int KPR = NW * KPW;                   // keys of the workgroup per round
+    __shared__ bf16x8 Qs[NRB * KF * 64];
+
+    const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, hf = lane >> 5;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
+    float* part_g = part + ((size_t)l * Hkv + g) * T;
+    const int key0 = split * keys_per_split;
+    const int key1 = min(T, key0 + keys_per_split);
+    bf16x8 ones = {};
+    if (hf == 0) ones[0] = ones[1] = ones[2] = (__bf16)1.0f;
+
+    bf16x8 kf[NKB][KS];
+    auto load_k = [&](bf16x8 (&dst)[NKB][KS], int kr) {
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            const int key = min(kr + 32 * kb + r32, T - 1);     // keys past T: never stored
+            const bf16x8* kp = (const bf16x8*)(Kg + (size_t)key * D + hf * 8);
+#pragma unroll
+            for (int j = 0; j < KS; ++j) dst[kb][j] = kp[2 * j];
         }
+    };
+
+    for (int rc0 = 0; rc0 < rows_pad; rc0 += NRB * 32) {
+        const int nrb = min(NRB, (rows_pad - rc0) / 32);
+        __syncthreads();                             // the previous chunk's reads are done
+        for (int f = tid; f < nrb * KF * 64; f += NW * 64) {
+            const int ln = f & 63, fj = f >> 6, rb = fj / KF, j = fj - rb * KF;
+            const int row = rc0 + rb * 32 + (ln & 31), h2 = ln >> 5;
+            bf16x8 v = {};
+            if (j < KS) {
+                if (row < n_rows) {
+                    const int t = row / G, hh = row - (row / G) * G;
+                    v = *(const bf16x8*)(q + (((size_t)l * Qn + t) * H + g * G + hh) * D +
+                                         16 * j + 8 * h2);
+                }
+            } else if (h2 == 0) {
+                const float x = row >= n_rows ? INFINITY
+                                : q_lse ? q_lse[((size_t)l * Qn + row / G) * H + g * G + row % G] * kLog2e
+                                        : lse2[((size_t)l * Hkv + g) * rows_pad + row];
+                const float y = -x / sl2;
+                if (fabsf(y) < INFINITY) {
+                    const uint16_t b1 = f32_to_bf16_bits(y);
+                    const float r1 = y - bf16_bits_to_f32(b1);
+                    const uint16_t b2 = f32_to_bf16_bits(r1);
+                    const uint16_t b3 = f32_to_bf16_bits(r1 - bf16_bits_to_f32(b2));
+                    v[0] = __builtin_bit_cast(__bf16, b1);
+                    v[1] = __builtin_bit_cast(__bf16, b2);
+                    v[2] = __builtin_bit_cast(__bf16, b3);
+                } else {
+                    v[0] = __builtin_bit_cast(__bf16, f32_to_bf16_bits(y));   // -inf: row adds 0
+                }
+            }
+            Qs[f] = v;
+        }
+        __syncthreads();
+
+        // One round: the wave's NKB key blocks (in kfr) against every row block;
+        // hook(rb) runs after the MFMAs of row block rb (before its exp2 work).
+        auto round = [&](const bf16x8 (&kfr)[NKB][KS], int kr, auto&& hook) {
+            float cs[NKB][2];
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) cs[kb][0] = cs[kb][1] = 0.f;
+#pragma unroll
+            for (int rb = 0; rb < NRB; ++rb) {
+                if (rb >= nrb) break;
+                f32x16 acc[NKB];
+                const bf16x8* qb = Qs + rb * KF * 64 + lane;
+#pragma unroll
+                for (int j = 0; j < KF; ++j) {
+                    const bf16x8 qj = qb[j * 64];
+#pragma unroll
+                    for (int kb = 0; kb < NKB; ++kb)
+                        acc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            qj, j < KS ? kfr[kb][j] : ones, j == 0 ? f32x16{} : acc[kb], 0, 0, 0);
+                }
+                hook(rb);
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) cs[kb][v & 1] += fast_exp2(acc[kb][v] * sl2);
+            }
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) {
+                const float s = pair_add(cs[kb][0] + cs[kb][1]);
+                const int key = kr + 32 * kb + r32;
+                if (hf == 0 && key < key1) part_g[key] = rc0 == 0 ? s : part_g[key] + s;
+            }
+        };
+
+        int kr = key0 + w * KPW;
+        if (kr < key1) load_k(kf, kr);
+        for (; kr < key1; kr += KPR)
+            round(kf, kr, [&](int rb) { if (rb == nrb - 1 && kr + KPR < key1) load_k(kf, kr + KPR); });
     }
 }
 
@@ -528,15 +604,18 @@ void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char*
     const dim3 block(NW * 64);
     const dim3 grid(w.n_split, p.H_kv, p.L);
     if (!p.q_lse) {
-        hipLaunchKernelGGL((score_pass_bf16<D, NW, true>), grid, block, 0, st, q, kc, p.T_c,
-                           p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2, stats,
-                           (const float*)nullptr, (const float*)nullptr, part);
+        hipLaunchKernelGGL((score_stats_bf16<D, NW>), grid, block, 0, st, q, kc, p.T_c,
+                           p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2, stats);
         const long n = (long)p.L * p.H_kv * w.rows_pad;
         hipLaunchKernelGGL(score_merge, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                            (const float2*)stats, p.L * p.H_kv, w.n_split, w.rows_pad, n_rows, lse2);
     }
-    hipLaunchKernelGGL((score_pass_bf16<D, NW, false>), grid, block, 0, st, q, kc, p.T_c,
-                       p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2, stats,
+    constexpr int KNW = RELAXKV_SCORE_KREG_NW, KNKB = RELAXKV_SCORE_KREG_NKB;
+    constexpr int kpr = KNW * KNKB * 32;                  // keys of a column-sum round
+    const int kps = (kKeysPerSplit + kpr - 1) / kpr * kpr;
+    const dim3 kgrid((p.T_c + kps - 1) / kps, p.H_kv, p.L);
+    hipLaunchKernelGGL((score_colsum_kreg<D, KNW, KNKB>), kgrid, dim3(KNW * 64), 0, st, q, kc,
+                       p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, kps, sl2,
                        (const float*)lse2, p.q_lse, part);
 }
 
