@@ -3,19 +3,17 @@
 //   p_{l,i} = (1/(H Qn)) sum_{h,t} A_l[h,t,i],   a_{l,i} = MinMax_i(p_{l,i}).
 //
 // bf16 path (bf16 MFMA, fp32 accumulation).  Per layer l and KV head g the
-// Qn*G query rows that share g form one row set; workgroups take splits of
-// 4096 contiguous keys:
-//   1. score_stats_bf16 -- each wave holds one 32-row block of the row set's
-//      queries in registers while 16 KB tiles of K stream through a ring of
-//      LDS buffers (direct global->LDS loads); S^T = K Q^T (one query row per
-//      lane) gives each row's (max, sum of exp2) over the split.
-//                                                        [skipped with q_lse]
+// Qn*G query rows that share g form one row set.  A workgroup takes one
+// (l, g, split of 4096 contiguous keys): it stages the row set into LDS once
+// (fragment-major), and each of its waves loads its own 32-key blocks from HBM
+// straight into registers and runs every 32-row block against them, so a query
+// fragment read from LDS feeds two MFMAs and K never passes through LDS:
+//   1. score_stats_kreg -- S^T = K Q^T (one query row per lane): each row's
+//      (reference, sum of exp2) over the split.           [skipped with q_lse]
 //   2. score_merge  -- per row, merge the splits into a log2-sum-exp.
-//   3. score_colsum_kreg -- the row set is staged once into LDS with each
-//      row's -lse as an extra k-step; each wave loads its own keys from HBM
-//      straight into registers and runs every row block against them
-//      (S = Q K^T - lse, one key per lane), summing exp2 over the rows: the
-//      pooled mass of each key for this KV head.
+//   3. score_colsum_kreg -- S = Q K^T - lse (one key per lane; the row's -lse
+//      rides as an extra k-step), summing exp2 over the rows: the pooled mass
+//      of each key for this KV head.
 //   4. score_pool / score_minmax -- the fixed-order sum over KV heads and the
 //      1/(H Qn) factor with per-block extrema, then the MinMax normalisation.
 // float32 path: plain VALU kernels with the same four steps (used for fp32
@@ -25,48 +23,28 @@
 
 #include <math.h>
 
-#include <type_traits>
-
 #include "dev_common.h"
 #include "internal.h"
 
 namespace relaxkv {
 namespace {
 
-constexpr int kTileBytes = 16384;             // bytes of K per LDS tile (64 keys at d = 128)
 #ifndef RELAXKV_SCORE_SPLIT
 #define RELAXKV_SCORE_SPLIT 4096              // keys per workgroup
 #endif
-#ifndef RELAXKV_SCORE_KRING
-#define RELAXKV_SCORE_KRING 4                 // K fragments read ahead of their MFMA
-#endif
-constexpr int kKeysPerSplit = RELAXKV_SCORE_SPLIT;
-constexpr int kMaxWaves = 10;                 // 32-row query blocks per workgroup (one per wave)
-#ifndef RELAXKV_SCORE_STAGES
-#define RELAXKV_SCORE_STAGES 3                // LDS ring of K tiles
-#endif
-#ifndef RELAXKV_SCORE_WPE
-#define RELAXKV_SCORE_WPE 3                   // waves per SIMD the schedule is made for
-#endif
-constexpr int kStages = RELAXKV_SCORE_STAGES;
 #ifndef RELAXKV_SCORE_KREG_NW
-#define RELAXKV_SCORE_KREG_NW 8               // waves per workgroup of that pass
+#define RELAXKV_SCORE_KREG_NW 8               // waves per workgroup
 #endif
 #ifndef RELAXKV_SCORE_KREG_NKB
 #define RELAXKV_SCORE_KREG_NKB 2              // 32-key blocks per wave and round
 #endif
+constexpr int kKeysPerSplit = RELAXKV_SCORE_SPLIT;
 constexpr int kKregRowBlocks = 10;            // 32-row blocks staged per row chunk
-constexpr int kRing = RELAXKV_SCORE_KRING;
 
 // Range a block's sum of exp2(s - m) may take before the statistics pass moves
-// its reference m (see score_stats_bf16).
+// its reference m (see score_stats_kreg).
 constexpr float kRefHi = 18446744073709551616.0f;     // 2^64
 constexpr float kRefLo = 5.42101086242752217e-20f;    // 2^-64
-
-template <int D>
-constexpr int tile_keys() { return kTileBytes / (2 * D); }
-
-constexpr int pow2_ceil(int x) { return x <= 1 ? 1 : 2 * pow2_ceil((x + 1) / 2); }
 
 __host__ __device__ inline int round_up32(int x) { return (x + 31) / 32 * 32; }
 
@@ -85,196 +63,62 @@ __device__ __forceinline__ float pair_other(float x) {
     return __uint_as_float(r[0] ^ r[1] ^ u);
 }
 
-// Row statistics over the keys of a split for the row set (l, g).  NW waves
-// each hold one 32-row block of the row set's queries in registers (row
-// rho = t*G + hh reads q[l][t][g*G + hh][:]); logits in log2 units are
-// sl2 = scale * log2(e) times the MFMA's dot products, applied in fp32.  16 KB
-// tiles of K stream into a ring of kStages swizzled LDS buffers by direct
-// global->LDS loads, kStages-1 tiles ahead of the MFMAs; the first NL/LPW waves
-// issue LPW loads per tile each, so one in-order count per wave says which tile
-// has landed.  S^T = K Q^T (one query row per lane, 16 keys per block): each
-// lane sums exp2(s - m) over its keys against a reference m that starts at 0
-// and moves to the block maximum only when a block's sum leaves [2^-64, 2^64]
-// (the rescale keeps the sum exact; until some lane of the wave moves, m = 0
-// costs no subtraction); merged with the lane 32 away ->
-// stats[l][g][split][row] = (m, sum) in log2 units, i.e. the row's sum of exp2
-// over the split is sum * 2^m.  Every logit costs one multiply, one exp2 and
-// one add.
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(RELAXKV_SCORE_WPE, RELAXKV_SCORE_WPE))) void score_stats_bf16(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
-    int Hkv, int G, int n_rows, int rows_pad, int n_split, float sl2,
-    float2* __restrict__ stats) {
-    constexpr int TK = tile_keys<D>();              // keys per tile
-    constexpr int NT = kKeysPerSplit / TK;          // tiles per split
+// Stage rows rc0 .. rc0 + 32 nrb - 1 of the row set (l, g) into Qs, fragment-major:
+// fragment (rb, j) holds the MFMA operand of 32-row block rb and k-step j (lane
+// l: row 32 rb + l % 32, 16-byte chunk 2j + l / 32; padding rows are zero).
+// With LSE, k-step KS of each block carries -lse2 / sl2 of the lane's row as
+// three bf16 terms in its first three k-slots (lanes 0-31; zero elsewhere).
+template <int D, int NW, bool LSE>
+__device__ __forceinline__ void stage_rows(bf16x8* Qs, const uint16_t* __restrict__ q, int l,
+                                           int g, int Qn, int H, int Hkv, int G, int n_rows,
+                                           int rows_pad, int rc0, int nrb, float sl2,
+                                           const float* __restrict__ lse2,
+                                           const float* __restrict__ q_lse) {
     constexpr int KS = D / 16;
-    constexpr int NB = TK / 32;                     // 32-key MFMA blocks per tile
-    constexpr int ROWB = 2 * D;                     // tile row bytes
-    constexpr int CH = D / 8;                       // 16-byte chunks per row
-    constexpr int RPI = 64 / CH;                    // rows per wave-wide load
-    constexpr int NL = TK / RPI;                    // wave-wide loads per tile (16)
-    constexpr int LPW = pow2_ceil((NL + NW - 1) / NW);   // loads per tile of a loading wave
-    constexpr int NLW = NL / LPW;                   // loading waves
-    constexpr int KA = kRing < KS ? kRing : KS;
-    static_assert(NL % LPW == 0 && NLW <= NW && kStages >= 2 && kStages <= 5 && TK % 64 == 0 &&
-                  NB % 2 == 0, "pipeline shape");
-    static_assert(RPI * ROWB == 1024, "one wave-wide load fills 1 KB");
-    __shared__ __attribute__((aligned(1024))) uint16_t Ks[kStages][TK * D];
-
-    const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
-    const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, hf = lane >> 5;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
-    const int key0 = split * kKeysPerSplit;
-    const int ntile = min(NT, (T - key0 + TK - 1) / TK);
-    const bool loader = w < NLW;
-
-    // Tile tt goes to stage tt % kStages.  Loading wave w issues loads
-    // j = w*LPW .. w*LPW + LPW-1; lane l of load j fills tile row j*RPI + l/CH at
-    // physical chunk l%CH, which holds logical chunk (l%CH) ^ swz(row).  Rows
-    // past T re-read row T-1; their logits are masked.
-    const int lrow = lane / CH, pchunk = lane % CH;
-    uint32_t loff[LPW];
-#pragma unroll
-    for (int i = 0; i < LPW; ++i) {
-        const int row = (w * LPW + i) * RPI + lrow;
-        loff[i] = (uint32_t)(row * ROWB + ((pchunk ^ tile_swz<D>(row)) << 4));
+    constexpr int KF = LSE ? KS + 1 : KS;
+    for (int f = threadIdx.x; f < nrb * KF * 64; f += NW * 64) {
+        const int ln = f & 63, fj = f >> 6, rb = fj / KF, j = fj - rb * KF;
+        const int row = rc0 + rb * 32 + (ln & 31), h2 = ln >> 5;
+        bf16x8 v = {};
+        if (j < KS) {
+            if (row < n_rows) {
+                const int t = row / G, hh = row - (row / G) * G;
+                v = *(const bf16x8*)(q + (((size_t)l * Qn + t) * H + g * G + hh) * D + 16 * j +
+                                     8 * h2);
+            }
+        } else if (h2 == 0) {
+            const float x = row >= n_rows ? INFINITY
+                            : q_lse ? q_lse[((size_t)l * Qn + row / G) * H + g * G + row % G] * kLog2e
+                                    : lse2[((size_t)l * Hkv + g) * rows_pad + row];
+            const float y = -x / sl2;
+            if (fabsf(y) < INFINITY) {
+                const uint16_t b1 = f32_to_bf16_bits(y);
+                const float r1 = y - bf16_bits_to_f32(b1);
+                const uint16_t b2 = f32_to_bf16_bits(r1);
+                const uint16_t b3 = f32_to_bf16_bits(r1 - bf16_bits_to_f32(b2));
+                v[0] = __builtin_bit_cast(__bf16, b1);
+                v[1] = __builtin_bit_cast(__bf16, b2);
+                v[2] = __builtin_bit_cast(__bf16, b3);
+            } else {
+                v[0] = __builtin_bit_cast(__bf16, f32_to_bf16_bits(y));   // -inf: row adds 0
+            }
+        }
+        Qs[f] = v;
     }
-    auto issue_tile = [&](int tt) {
-        if (!loader) return;
-        const uint32_t st = lds_addr(Ks[tt % kStages]) + (uint32_t)(w * LPW) * 1024u;
-        const int kb = key0 + tt * TK;
-        const char* tb = (const char*)(Kg + (size_t)kb * D);
-        const bool tail = kb + TK > T;
-#pragma unroll
-        for (int i = 0; i < LPW; ++i) {
-            uint32_t o = loff[i];
-            if (tail) {                                  // clamp the row to T-1
-                int row = (w * LPW + i) * RPI + lrow;
-                asm volatile("" : "+v"(row));
-                o = (uint32_t)(min(row, T - 1 - kb) * ROWB) + (o & (ROWB - 1));
-            }
-            fill_lds16(tb + o, st + (uint32_t)i * 1024u);
-        }
-    };
-    // Wait for tile tt (rem tiles were issued after it), then barrier.
-    auto wait_tile = [&](int rem) {
-        if (kStages >= 5 && rem >= 3) wait_loads_barrier<(kStages >= 5 ? 3 : 0) * LPW>();
-        else if (kStages >= 4 && rem >= 2) wait_loads_barrier<(kStages >= 4 ? 2 : 0) * LPW>();
-        else if (kStages >= 3 && rem >= 1) wait_loads_barrier<LPW>();
-        else wait_loads_barrier<0>();
-    };
-    // K fragment (tile row 32b + r32, logical chunk 2ks + hf) byte offset.
-    const int k_base = r32 * ROWB | ((hf ^ tile_swz<D>(r32)) << 4);
+}
 
-    for (int rc0 = 0; rc0 < rows_pad; rc0 += NW * 32) {
-        const int rho = rc0 + w * 32 + r32;
-        bf16x8 qf[KS];
-        if (rho < n_rows) {
-            const int t = rho / G, hh = rho % G;
-            const uint16_t* qrow = q + (((size_t)l * Qn + t) * H + g * G + hh) * D;
+// The 32-key blocks kr + 32 kb (kb < NKB) of K into registers, as MFMA operands
+// (lane l: key kr + 32 kb + l % 32, 16-byte chunk 2j + l / 32 of k-step j); keys
+// past T re-read key T-1 (their results are masked or never stored).
+template <int D, int NKB>
+__device__ __forceinline__ void load_keys(bf16x8 (&dst)[NKB][D / 16], const uint16_t* Kg, int T,
+                                          int kr, int r32, int hf) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
-        } else {
+    for (int kb = 0; kb < NKB; ++kb) {
+        const int key = min(kr + 32 * kb + r32, T - 1);
+        const bf16x8* kp = (const bf16x8*)(Kg + (size_t)key * D + hf * 8);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) qf[ks] = bf16x8{};
-        }
-        float m_ref = 0.f, z_run = 0.f;
-        bool moved = false;             // some lane of the wave left reference 0
-        __syncthreads();                // LDS free from the previous row chunk
-
-        // KS MFMAs of block (tt, b) into acc, K fragments read KA ahead.
-        auto mfma_block = [&](int tt, int b, f32x16& acc) {
-            int kbo = k_base;
-            asm volatile("" : "+v"(kbo));
-            const char* kp = (const char*)Ks[tt % kStages] + b * 32 * ROWB;
-            bf16x8 kf[KA];
-#pragma unroll
-            for (int i = 0; i < KA; ++i) kf[i] = *(const bf16x8*)(kp + (kbo ^ (i << 5)));
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 cur = kf[ks % KA];
-                if (ks + KA < KS) kf[ks % KA] = *(const bf16x8*)(kp + (kbo ^ ((ks + KA) << 5)));
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[ks], ks > 0 ? acc : f32x16{},
-                                                              0, 0, 0);
-            }
-        };
-        // Sum of exp2(sl2 * acc) over a block (minus m_ref when SUB).
-        auto exp_sum = [&](const f32x16& acc, auto sub) {
-            float z0 = 0.f, z1 = 0.f;
-#pragma unroll
-            for (int v = 0; v < 16; v += 2) {
-                if constexpr (decltype(sub)::value) {
-                    z0 += fast_exp2(fmaf(acc[v], sl2, -m_ref));
-                    z1 += fast_exp2(fmaf(acc[v + 1], sl2, -m_ref));
-                } else {
-                    z0 += fast_exp2(acc[v] * sl2);
-                    z1 += fast_exp2(acc[v + 1] * sl2);
-                }
-            }
-            return z0 + z1;
-        };
-        // Block key base kb0: mask keys past T (acc[v] is key
-        // kb0 + 8(v/4) + 4hf + v%4 of row rho).
-        auto mask_tail = [&](int kb0, f32x16& acc) {
-            if (kb0 + 32 > T) {
-#pragma unroll
-                for (int v = 0; v < 16; ++v)
-                    if (kb0 + 8 * (v >> 2) + 4 * hf + (v & 3) >= T) acc[v] = -INFINITY;
-            }
-        };
-        // The vector work of block (tt, b) held in acc: fold the block's sum
-        // into the row's running sum, moving the reference when the block's sum
-        // leaves [2^-64, 2^64] (rare).
-        auto consume = [&](int tt, int b, f32x16& acc) {
-            {
-                mask_tail(key0 + tt * TK + 32 * b, acc);
-                float zb = moved ? exp_sum(acc, std::true_type{}) : exp_sum(acc, std::false_type{});
-                const bool out = !(zb <= kRefHi) || z_run + zb < kRefLo;
-                if (__builtin_expect(out, 0)) {
-                    // New reference: the larger of the block maximum and the
-                    // log2 of what the row has summed so far, so neither the
-                    // block's terms nor the running sum exceed 16 times it.
-                    float mt = acc[0];
-#pragma unroll
-                    for (int v = 1; v < 16; ++v) mt = fmaxf(mt, acc[v]);
-                    mt *= sl2;
-                    const float lz = z_run > 0.f ? m_ref + __log2f(z_run) : -INFINITY;
-                    mt = fmaxf(mt, lz);
-                    if (mt > -INFINITY) {
-                        zb = 0.f;
-#pragma unroll
-                        for (int v = 0; v < 16; ++v) zb += fast_exp2(fmaf(acc[v], sl2, -mt));
-                        z_run = fast_exp2(lz - mt);          // the running sum rescaled (<= 1)
-                        m_ref = mt;
-                    }
-                }
-                moved = moved || __any(out);
-                z_run += zb;
-            }
-        };
-
-        f32x16 acc[NB];
-#pragma unroll
-        for (int tt = 0; tt < kStages - 1; ++tt)
-            if (tt < ntile) issue_tile(tt);
-        for (int tt = 0; tt < ntile; ++tt) {
-            // Tile tt has landed and every wave is past tile tt-1 (whose stage
-            // the next fill reuses).
-            wait_tile(min(kStages - 2, ntile - 1 - tt));
-            if (tt + kStages - 1 < ntile) issue_tile(tt + kStages - 1);
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                mfma_block(tt, b, acc[b]);
-                consume(tt, b, acc[b]);
-            }
-        }
-        // merge with the lane 32 away (same row, the other half of the keys)
-        const float m2 = pair_other(m_ref), z2 = pair_other(z_run);
-        const float M = fmaxf(m_ref, m2);
-        const float Z = z_run * fast_exp2(m_ref - M) + z2 * fast_exp2(m2 - M);
-        if (hf == 0 && rho < rows_pad)
-            stats[(((size_t)l * Hkv + g) * n_split + split) * rows_pad + rho] = make_float2(M, Z);
+        for (int j = 0; j < D / 16; ++j) dst[kb][j] = kp[2 * j];
     }
 }
 
@@ -318,48 +162,12 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
     if (hf == 0) ones[0] = ones[1] = ones[2] = (__bf16)1.0f;
 
     bf16x8 kf[NKB][KS];
-    auto load_k = [&](bf16x8 (&dst)[NKB][KS], int kr) {
-#pragma unroll
-        for (int kb = 0; kb < NKB; ++kb) {
-            const int key = min(kr + 32 * kb + r32, T - 1);     // keys past T: never stored
-            const bf16x8* kp = (const bf16x8*)(Kg + (size_t)key * D + hf * 8);
-#pragma unroll
-            for (int j = 0; j < KS; ++j) dst[kb][j] = kp[2 * j];
-        }
-    };
+    auto load_k = [&](bf16x8 (&dst)[NKB][KS], int kr) { load_keys<D, NKB>(dst, Kg, T, kr, r32, hf); };
 
     for (int rc0 = 0; rc0 < rows_pad; rc0 += NRB * 32) {
         const int nrb = min(NRB, (rows_pad - rc0) / 32);
         __syncthreads();                             // the previous chunk's reads are done
-        for (int f = tid; f < nrb * KF * 64; f += NW * 64) {
-            const int ln = f & 63, fj = f >> 6, rb = fj / KF, j = fj - rb * KF;
-            const int row = rc0 + rb * 32 + (ln & 31), h2 = ln >> 5;
-            bf16x8 v = {};
-            if (j < KS) {
-                if (row < n_rows) {
-                    const int t = row / G, hh = row - (row / G) * G;
-                    v = *(const bf16x8*)(q + (((size_t)l * Qn + t) * H + g * G + hh) * D +
-                                         16 * j + 8 * h2);
-                }
-            } else if (h2 == 0) {
-                const float x = row >= n_rows ? INFINITY
-                                : q_lse ? q_lse[((size_t)l * Qn + row / G) * H + g * G + row % G] * kLog2e
-                                        : lse2[((size_t)l * Hkv + g) * rows_pad + row];
-                const float y = -x / sl2;
-                if (fabsf(y) < INFINITY) {
-                    const uint16_t b1 = f32_to_bf16_bits(y);
-                    const float r1 = y - bf16_bits_to_f32(b1);
-                    const uint16_t b2 = f32_to_bf16_bits(r1);
-                    const uint16_t b3 = f32_to_bf16_bits(r1 - bf16_bits_to_f32(b2));
-                    v[0] = __builtin_bit_cast(__bf16, b1);
-                    v[1] = __builtin_bit_cast(__bf16, b2);
-                    v[2] = __builtin_bit_cast(__bf16, b3);
-                } else {
-                    v[0] = __builtin_bit_cast(__bf16, f32_to_bf16_bits(y));   // -inf: row adds 0
-                }
-            }
-            Qs[f] = v;
-        }
+        stage_rows<D, NW, true>(Qs, q, l, g, Qn, H, Hkv, G, n_rows, rows_pad, rc0, nrb, sl2, lse2, q_lse);
         __syncthreads();
 
         // One round: the wave's NKB key blocks (in kfr) against every row block;
@@ -399,6 +207,150 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
         if (kr < key1) load_k(kf, kr);
         for (; kr < key1; kr += KPR)
             round(kf, kr, [&](int rb) { if (rb == nrb - 1 && kr + KPR < key1) load_k(kf, kr + KPR); });
+    }
+}
+
+// Row statistics with the keys in registers: the same workgroup shape, staging
+// and key rounds as score_colsum_kreg, with S^T = K Q^T (K the A operand from
+// registers, the staged query fragment the B operand), so lane l holds row
+// 32 rb + l % 32 and 16 keys of each 32-key block.  Per row block each lane
+// keeps (m, z) = (reference, sum of exp2(s - m)) in log2 units over its keys,
+// with a lazy reference: m starts at 0 and moves only when a block's sum
+// leaves [2^-64, 2^64], to the larger of the block maximum and log2 of the
+// running sum (so no term and no running sum exceeds 16 * 2^m); until some lane
+// of the wave moves, m = 0 costs no subtraction.  Logits hundreds of log2 units
+// from 0 (either sign) stay exact.  At the end of a row chunk the two
+// half-waves and then the NW waves are merged in a fixed order (through LDS)
+// into stats[l][g][split][row].
+template <int D, int NW, int NKB>
+__global__ __launch_bounds__(NW * 64) void score_stats_kreg(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
+    int Hkv, int G, int n_rows, int rows_pad, int keys_per_split, int n_split, float sl2,
+    float2* __restrict__ stats) {
+    constexpr int KS = D / 16;
+    constexpr int NRB = kKregRowBlocks;
+    constexpr int KPW = NKB * 32;
+    constexpr int KPR = NW * KPW;
+    __shared__ bf16x8 Qs[NRB * KS * 64];
+    __shared__ float2 red[NW][NRB * 32];
+
+    const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, hf = lane >> 5;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
+    const int key0 = split * keys_per_split;
+    const int key1 = min(T, key0 + keys_per_split);
+    bf16x8 kf[NKB][KS];
+
+    for (int rc0 = 0; rc0 < rows_pad; rc0 += NRB * 32) {
+        const int nrb = min(NRB, (rows_pad - rc0) / 32);
+        __syncthreads();                             // the previous chunk's reads are done
+        stage_rows<D, NW, false>(Qs, q, l, g, Qn, H, Hkv, G, n_rows, rows_pad, rc0, nrb, sl2,
+                                 nullptr, nullptr);
+        __syncthreads();
+
+        float m_ref[NRB], z_run[NRB];
+        bool moved[NRB];                             // some lane of the wave left reference 0
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+            m_ref[rb] = 0.f;
+            z_run[rb] = 0.f;
+            moved[rb] = false;
+        }
+        int kr = key0 + w * KPW;
+        if (kr < key1) load_keys<D, NKB>(kf, Kg, T, kr, r32, hf);
+        for (; kr < key1; kr += KPR) {
+#pragma unroll
+            for (int rb = 0; rb < NRB; ++rb) {
+                if (rb < nrb) {
+                    f32x16 acc[NKB];
+                    const bf16x8* qb = Qs + rb * KS * 64 + lane;
+#pragma unroll
+                    for (int j = 0; j < KS; ++j) {
+                        const bf16x8 qj = qb[j * 64];
+#pragma unroll
+                        for (int kb = 0; kb < NKB; ++kb)
+                            acc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                kf[kb][j], qj, j == 0 ? f32x16{} : acc[kb], 0, 0, 0);
+                    }
+                    if (rb == nrb - 1 && kr + KPR < key1)
+                        load_keys<D, NKB>(kf, Kg, T, kr + KPR, r32, hf);
+#pragma unroll
+                    for (int kb = 0; kb < NKB; ++kb) {
+                        // acc[kb][v] is key kr + 32 kb + 8(v/4) + 4 hf + v%4 of the row.
+                        const int kb0 = kr + 32 * kb;
+                        if (kb0 + 32 > key1) {
+#pragma unroll
+                            for (int v = 0; v < 16; ++v)
+                                if (kb0 + 8 * (v >> 2) + 4 * hf + (v & 3) >= key1)
+                                    acc[kb][v] = -INFINITY;
+                        }
+                        float z0 = 0.f, z1 = 0.f;
+                        if (moved[rb]) {
+                            const float m = m_ref[rb];
+#pragma unroll
+                            for (int v = 0; v < 16; v += 2) {
+                                z0 += fast_exp2(fmaf(acc[kb][v], sl2, -m));
+                                z1 += fast_exp2(fmaf(acc[kb][v + 1], sl2, -m));
+                            }
+                        } else {
+#pragma unroll
+                            for (int v = 0; v < 16; v += 2) {
+                                z0 += fast_exp2(acc[kb][v] * sl2);
+                                z1 += fast_exp2(acc[kb][v + 1] * sl2);
+                            }
+                        }
+                        float zb = z0 + z1;
+                        const bool out = !(zb <= kRefHi) || z_run[rb] + zb < kRefLo;
+                        if (__builtin_expect(out, 0)) {
+                            // New reference: the larger of the block maximum and the
+                            // log2 of what the row has summed so far.
+                            float mt = acc[kb][0];
+#pragma unroll
+                            for (int v = 1; v < 16; ++v) mt = fmaxf(mt, acc[kb][v]);
+                            mt *= sl2;
+                            const float lz =
+                                z_run[rb] > 0.f ? m_ref[rb] + __log2f(z_run[rb]) : -INFINITY;
+                            mt = fmaxf(mt, lz);
+                            if (mt > -INFINITY) {
+                                zb = 0.f;
+#pragma unroll
+                                for (int v = 0; v < 16; ++v)
+                                    zb += fast_exp2(fmaf(acc[kb][v], sl2, -mt));
+                                z_run[rb] = fast_exp2(lz - mt);
+                                m_ref[rb] = mt;
+                            }
+                        }
+                        moved[rb] = moved[rb] || __any(out);
+                        z_run[rb] += zb;
+                    }
+                }
+            }
+        }
+        // Each half-wave's (m, z) per row; a half that met no key holds (0, 0)
+        // and becomes (-inf, 0), so no merge takes its 0 as the reference.
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+            if (rb < nrb) {
+                const float m = z_run[rb] > 0.f ? m_ref[rb] : -INFINITY, z = z_run[rb];
+                const float m2 = pair_other(m), z2 = pair_other(z);
+                const float M = fmaxf(m, m2);
+                const float Z = M == -INFINITY ? 0.f : z * fast_exp2(m - M) + z2 * fast_exp2(m2 - M);
+                if (hf == 0) red[w][rb * 32 + r32] = make_float2(M, Z);
+            }
+        }
+        __syncthreads();
+        for (int row = tid; row < nrb * 32; row += NW * 64) {
+            float M = -INFINITY;
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, red[ww][row].x);
+            float Z = 0.f;
+            if (M > -INFINITY) {
+#pragma unroll
+                for (int ww = 0; ww < NW; ++ww) Z += red[ww][row].y * fast_exp2(red[ww][row].x - M);
+            }
+            stats[(((size_t)l * Hkv + g) * n_split + split) * rows_pad + rc0 + row] = make_float2(M, Z);
+        }
     }
 }
 
@@ -591,7 +543,7 @@ void launch_finalize(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws
     hipLaunchKernelGGL(score_minmax, grid, dim3(256), 0, st, (const float2*)mm, w.n_blk, p.T_c, scores);
 }
 
-template <int D, int NW>
+template <int D>
 void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws,
                         hipStream_t st, float sl2) {
     const int G = p.H / p.H_kv;
@@ -601,19 +553,19 @@ void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char*
     float* part = (float*)(ws + w.part_off);
     float* lse2 = (float*)(ws + w.lse_off);
     float2* stats = (float2*)(ws + w.stats_off);
-    const dim3 block(NW * 64);
-    const dim3 grid(w.n_split, p.H_kv, p.L);
+    constexpr int KNW = RELAXKV_SCORE_KREG_NW, KNKB = RELAXKV_SCORE_KREG_NKB;
+    constexpr int kpr = KNW * KNKB * 32;                  // keys of a round
+    static_assert(kKeysPerSplit % kpr == 0, "the statistics splits are the workspace's n_split");
+    const int kps = kKeysPerSplit;
+    const dim3 kgrid((p.T_c + kps - 1) / kps, p.H_kv, p.L);
     if (!p.q_lse) {
-        hipLaunchKernelGGL((score_stats_bf16<D, NW>), grid, block, 0, st, q, kc, p.T_c,
-                           p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, w.n_split, sl2, stats);
+        hipLaunchKernelGGL((score_stats_kreg<D, KNW, KNKB>), kgrid, dim3(KNW * 64), 0, st, q, kc,
+                           p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, kps, w.n_split,
+                           sl2, stats);
         const long n = (long)p.L * p.H_kv * w.rows_pad;
         hipLaunchKernelGGL(score_merge, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                            (const float2*)stats, p.L * p.H_kv, w.n_split, w.rows_pad, n_rows, lse2);
     }
-    constexpr int KNW = RELAXKV_SCORE_KREG_NW, KNKB = RELAXKV_SCORE_KREG_NKB;
-    constexpr int kpr = KNW * KNKB * 32;                  // keys of a column-sum round
-    const int kps = (kKeysPerSplit + kpr - 1) / kpr * kpr;
-    const dim3 kgrid((p.T_c + kps - 1) / kps, p.H_kv, p.L);
     hipLaunchKernelGGL((score_colsum_kreg<D, KNW, KNKB>), kgrid, dim3(KNW * 64), 0, st, q, kc,
                        p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, kps, sl2,
                        (const float*)lse2, p.q_lse, part);
@@ -622,13 +574,7 @@ void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char*
 template <int D>
 hipError_t launch_score_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws,
                              float* scores, hipStream_t st, float scale) {
-    const float sl2 = scale * kLog2e;
-    // One wave per 32-row block of the row set, up to kMaxWaves; larger row sets
-    // loop over row chunks of kMaxWaves blocks.
-    const int nrb = w.rows_pad / 32;
-    if (nrb <= 4) launch_passes_bf16<D, 4>(p, w, ws, st, sl2);
-    else if (nrb <= 8) launch_passes_bf16<D, 8>(p, w, ws, st, sl2);
-    else launch_passes_bf16<D, kMaxWaves>(p, w, ws, st, sl2);
+    launch_passes_bf16<D>(p, w, ws, st, scale * kLog2e);
     launch_finalize(p, w, ws, scores, st);
     return hipGetLastError();
 }

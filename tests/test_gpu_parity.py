@@ -109,13 +109,15 @@ def test_supplied_lse_scoring(gpu_lib):
     assert_close(a_gpu, a_ref, w, "scores with supplied lse")
 
 
-@pytest.mark.parametrize("kind", ["large", "negative"])
-def test_scores_extreme_logits(gpu_lib, kind):
+@pytest.mark.parametrize("kind,T_c", [("large", 1500), ("negative", 1500), ("negative", 4097)])
+def test_scores_extreme_logits(gpu_lib, kind, T_c):
     """Logits far outside the unit range (tens to hundreds of log2 units): the
     row statistics must stay exact when a block's sum of exp2 would overflow
     fp32 ("large": spread of about +-150 log2 units) or underflow against the
-    starting reference ("negative": every logit near -500 log2 units)."""
-    w = synth.shrink(W["llama8b-8k"], L=2, T_c=1500, Qn=4)
+    starting reference ("negative": every logit near -500 log2 units).  At
+    T_c = 4097 the last 4096-key split holds one key, so half of each row's
+    lanes meet no key there and must not pull the merged reference to 0."""
+    w = synth.shrink(W["llama8b-8k"], L=2, T_c=T_c, Qn=4)
     case = Case(w)
     g = torch.Generator().manual_seed(7)
     if kind == "large":
