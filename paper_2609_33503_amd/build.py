@@ -36,7 +36,8 @@ def _hipcc():
 
 # The attention and scoring kernels never see NaN (masked logits are -inf):
 # without NaN semantics fmaxf needs no operand canonicalisation.
-PER_FILE = {"attn.hip": ["-fno-honor-nans"], "score.hip": ["-fno-honor-nans"]}
+PER_FILE = {"attn.hip": ["-fno-honor-nans"], "score.hip": ["-fno-honor-nans"],
+            "query_attn.hip": ["-fno-honor-nans"]}
 
 
 def _compile(src):

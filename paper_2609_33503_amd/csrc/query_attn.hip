@@ -28,7 +28,10 @@ namespace relaxkv {
 namespace {
 
 constexpr int kQaKeys = 64;            // keys per tile
-constexpr int kQaStages = 3;           // LDS ring depth (a K and a V tile per stage)
+#ifndef RELAXKV_QA_STAGES
+#define RELAXKV_QA_STAGES 4
+#endif
+constexpr int kQaStages = RELAXKV_QA_STAGES;   // LDS ring depth (a K and a V tile per stage)
 constexpr int kQaMinSplit = 256;       // fewest cache keys per split
 constexpr int kQaMaxSplit = 4096;      // most cache keys per split
 constexpr int kQaRing = 4;             // K fragments read ahead of their MFMA
@@ -70,7 +73,7 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
     constexpr int NL2 = 2 * NL;            // K and V
     constexpr int LPW = NL2 / NW;          // loads per tile every wave issues (some one more)
     constexpr int NI = (NL2 + NW - 1) / NW;
-    static_assert(LPW >= 1 && kQaStages == 3, "loader shape");
+    static_assert(LPW >= 1 && (kQaStages == 3 || kQaStages == 4), "loader shape");
     __shared__ __attribute__((aligned(1024))) uint16_t Kt[kQaStages][TK * D];
     __shared__ __attribute__((aligned(1024))) uint16_t Vt[kQaStages][TK * D];
 
@@ -132,8 +135,11 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
             }
         }
     };
+    // rem = tiles issued after the one needed now: each wave issued at least
+    // LPW loads per tile after it (in-order completion).
     auto wait_tile = [&](int rem) {
-        if (rem >= 1) wait_loads_barrier<LPW>();
+        if (kQaStages > 3 && rem >= 2) wait_loads_barrier<2 * LPW>();
+        else if (rem >= 1) wait_loads_barrier<LPW>();
         else wait_loads_barrier<0>();
     };
 
@@ -181,10 +187,14 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
                 if (32 + 8 * (v >> 2) + (v & 3) > e) s[1][v] = -INFINITY;
             }
         }
-        float m = fmaxf(s[0][0], s[1][0]);
+        // Two chains of 3-input maxima (two new values per instruction).
+        float m0 = fmaxf(s[0][0], s[0][1]), m1 = fmaxf(s[1][0], s[1][1]);
 #pragma unroll
-        for (int v = 1; v < 16; ++v) m = fmaxf(m, fmaxf(s[0][v], s[1][v]));
-        const float mx = qa_pair_max(m) * a.sl2;
+        for (int v = 2; v < 16; v += 2) {
+            m0 = fmaxf(fmaxf(m0, s[0][v]), s[0][v + 1]);
+            m1 = fmaxf(fmaxf(m1, s[1][v]), s[1][v + 1]);
+        }
+        const float mx = qa_pair_max(fmaxf(m0, m1)) * a.sl2;
         if (__any(mx > m_run + kQaSlack)) {
             const float m_new = mx > m_run + kQaSlack ? mx : m_run;
             const float alpha = fast_exp2(m_run - m_new);
@@ -193,17 +203,30 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
             for (int db = 0; db < DB; ++db) o[db] *= alpha;
             m_run = m_new;
         }
+        // The row sum adds the bf16 probabilities that the PV product uses, two
+        // per dot2 instruction, in four chains.
         bf16x8 pb[2][2];
-        float ls = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const float p = fast_exp2(fmaf(s[kb][v], a.sl2, -m_run));
-                ls += p;
-                pb[kb][v >> 3][v & 7] = (__bf16)p;
-            }
-        l_run += ls;
+            for (int v = 0; v < 16; ++v)
+                pb[kb][v >> 3][v & 7] = (__bf16)fast_exp2(fmaf(s[kb][v], a.sl2, -m_run));
+        {
+            typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+            const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+            float ls0 = 0.f, ls1 = 0.f, ls2 = 0.f, ls3 = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int k2 = 0; k2 < 2; ++k2) {
+                    const bf16x8 q8 = pb[kb][k2];
+                    ls0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(q8, q8, 0, 1), one2, ls0, false);
+                    ls1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(q8, q8, 2, 3), one2, ls1, false);
+                    ls2 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(q8, q8, 4, 5), one2, ls2, false);
+                    ls3 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(q8, q8, 6, 7), one2, ls3, false);
+                }
+            l_run += (ls0 + ls1) + (ls2 + ls3);
+        }
         // O^T += V^T P^T
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
