@@ -31,6 +31,9 @@ constexpr int kQaKeys = 64;            // keys per tile
 #ifndef RELAXKV_QA_STAGES
 #define RELAXKV_QA_STAGES 4
 #endif
+#ifndef RELAXKV_QA_WGS
+#define RELAXKV_QA_WGS 256                     // workgroups the key splits aim for (one per CU)
+#endif
 constexpr int kQaStages = RELAXKV_QA_STAGES;   // LDS ring depth (a K and a V tile per stage)
 constexpr int kQaMinSplit = 256;       // fewest cache keys per split
 constexpr int kQaMaxSplit = 4096;      // most cache keys per split
@@ -398,7 +401,7 @@ QueryAttnWorkspace query_attn_workspace_layout(const relaxkv_problem& p) {
     // One round of workgroups over the CUs: about 256 / (H_kv * chunks) splits,
     // each a multiple of the 64-key tile.
     const long groups = (long)p.H_kv * w.n_chunks;
-    const long want = groups >= 256 ? 1 : 256 / groups;
+    const long want = groups >= RELAXKV_QA_WGS ? 1 : RELAXKV_QA_WGS / groups;
     long kps = ((long)p.T_c + want - 1) / want;
     kps = (kps + kQaKeys - 1) / kQaKeys * kQaKeys;
     kps = kps < kQaMinSplit ? kQaMinSplit : kps > kQaMaxSplit ? kQaMaxSplit : kps;
