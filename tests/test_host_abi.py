@@ -236,3 +236,14 @@ def test_compute_calls_reject_before_launch(rk):
     c = (ctypes.c_int32 * 6)()
     assert lib.relaxkv_counts_to_host(None, c, None, None) == rk.EINVAL
     assert lib.relaxkv_counts_to_host(ctypes.byref(s), None, None, None) == rk.EINVAL
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: any other count exits with status 2 and says so
+    (before touching a device)."""
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr
