@@ -9,8 +9,8 @@
 //   (token t, head g*G + hh -> row t*G + hh) and one split of consecutive
 //   cache keys (sized on the host so that one round of workgroups covers the
 //   layer); the last split also takes the query tokens' own keys;
-// - K and V tiles of 64 keys stream into a 3-deep ring of swizzled LDS buffers
-//   by direct global->LDS loads (see tile_swz), two tiles ahead of the MFMAs;
+// - K and V tiles of 64 keys stream into a 4-deep ring of swizzled LDS buffers
+//   by direct global->LDS loads (see tile_swz), three tiles ahead of the MFMAs;
 // - each wave computes S^T = K Q^T for its 32 rows (one row per lane), a
 //   flash-style online softmax in the exp2 domain with lazy rescaling, and
 //   O^T += V^T P^T with transposing LDS reads of V;
