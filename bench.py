@@ -45,7 +45,7 @@ PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_qwen14b-32k-planted.traffic.json")
 KERNEL_SOURCES = ("paper_2609_33503_amd/csrc/attn.hip", "paper_2609_33503_amd/csrc/attn_config.h",
-                  "paper_2609_33503_amd/csrc/dev_common.h")
+                  "paper_2609_33503_amd/csrc/dev_common.h", "paper_2609_33503_amd/build.py")
 
 
 def measured_traffic(workload):

@@ -35,8 +35,11 @@ def _hipcc():
 
 
 # The attention and scoring kernels never see NaN (masked logits are -inf):
-# without NaN semantics fmaxf needs no operand canonicalisation.
-PER_FILE = {"attn.hip": ["-fno-honor-nans"], "score.hip": ["-fno-honor-nans"],
+# without NaN semantics fmaxf needs no operand canonicalisation.  The sparse
+# attention is scheduled with the backend's max-ILP strategy (about 2% faster on
+# the 32K workload than the default; the same instructions, reordered).
+PER_FILE = {"attn.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+            "score.hip": ["-fno-honor-nans"],
             "query_attn.hip": ["-fno-honor-nans"]}
 
 
