@@ -15,7 +15,7 @@ import torch
 from hypothesis import given, settings
 from hypothesis import strategies as st
 
-from oracle import anchor_count, build_sets, score, select, sparse_attn
+from oracle import anchor_count, attention_flops, build_sets, score, select, sparse_attn
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -80,6 +80,46 @@ def test_hand_example_attention():
         O, _ = sparse_attn(l, s, qn, kn, vn, kc, vc, softmax_scale=1.0,
                            mode=case["mode"], targets=[t])
         assert O[0, 0, 0] == pytest.approx(case["out"], abs=1e-12)
+
+
+def _count_attention_flops(sets, H, d, mode="union"):
+    """Operation count of a naive evaluation, enumerated from the mask itself
+    (not from the edge counts): for every layer, target p in R_l, query head
+    and context key j (j in U and j <= p, or j <= p for the full prefix) one
+    d-long dot product (d multiplies, d adds) and one d-long scaled
+    accumulation of V_j (d multiplies, d adds)."""
+    n = 0
+    union = set(sets.U.tolist())
+    for l in range(sets.L):
+        for p in sets.R[l].tolist():
+            for _h in range(H):
+                for j in range(p + 1):
+                    if mode == "full" or j in union:
+                        n += (d + d) + (d + d)
+    return n
+
+
+def test_attention_flops_hand_example():
+    # 10 + 9 + 5 = 24 unmasked edges (App. A.2 edge count); with one head and
+    # d = 1 each edge is one multiply-add for the logit and one for the output.
+    ex = _hand()
+    s = build_sets(np.array(ex["anchors"]), ex["T_c"])
+    assert attention_flops(1, 1, s.edges) == 96.0
+    assert attention_flops(1, 1, s.edges_full) == 4 * (18 + 16 + 8)
+    assert attention_flops(3, 5, s.edges) == _count_attention_flops(s, 3, 5)
+    assert attention_flops(3, 5, s.edges_full) == _count_attention_flops(s, 3, 5, "full")
+
+
+@settings(max_examples=40, deadline=None)
+@given(st.integers(1, 4), st.integers(1, 40), st.integers(1, 4), st.integers(1, 9),
+       st.integers(0, 2**31 - 1), st.data())
+def test_attention_flops_brute_force(L, T, H, d, seed, data):
+    k = data.draw(st.integers(1, T))
+    rng = np.random.default_rng(seed)
+    S = np.stack([np.sort(rng.choice(T, size=k, replace=False)) for _ in range(L)])
+    s = build_sets(S, T)
+    assert attention_flops(H, d, s.edges) == _count_attention_flops(s, H, d)
+    assert attention_flops(H, d, s.edges_full) == _count_attention_flops(s, H, d, "full")
 
 
 # ----------------------------------------------------------------------------
