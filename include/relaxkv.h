@@ -38,8 +38,18 @@
  *   float32) for Q/K/V and attention outputs.
  * - Layers are 0-based; positions are context positions 0 .. T_c-1 (the
  *   query tokens are never targets or context).
- * - Calls are stateless and reentrant; two calls that write the same buffers
- *   must be ordered by the caller.
+ * - The library keeps no state between calls and calls are reentrant; two
+ *   calls that write the same buffers must be ordered by the caller.  The one
+ *   piece of request state on the host is in relaxkv_sets: the set-building
+ *   calls record in it which kind of target and context lists they built
+ *   (global_targets, context_sets), so pass the struct the last of them
+ *   filled, not an older copy.  A stale copy cannot make a kernel overrun:
+ *   the attention and cache-update kernels clamp the device row count to the
+ *   row capacity they were given and to the bound the host sized their grid
+ *   from, and set RELAXKV_ERR_ROWS when they had to clamp.
+ * - Device error word (counts[L+1] of relaxkv_sets, cleared by relaxkv_select):
+ *   bits RELAXKV_ERR_*; relaxkv_counts_to_host returns RELAXKV_EINVAL while it
+ *   is nonzero.
  */
 #ifndef RELAXKV_H
 #define RELAXKV_H
@@ -57,6 +67,13 @@ typedef int32_t relaxkv_status;
 #define RELAXKV_ENOSPACE     -2  /* caller buffer smaller than the size query reports */
 #define RELAXKV_EUNSUPPORTED -3  /* head_dim, dtype or head layout this build has no kernel for */
 #define RELAXKV_EDEVICE      -4  /* a HIP runtime call or kernel launch failed */
+
+/* Bits of the device error word counts[L+1]. */
+#define RELAXKV_ERR_NAN_SCORE   1  /* a NaN score reached a selection */
+#define RELAXKV_ERR_BAD_TARGETS 2  /* relaxkv_build_sets_global got an invalid target list */
+#define RELAXKV_ERR_ROWS        4  /* |R_l| on the device exceeded the rows an attention or
+                                      cache-update call could process (its n_rows, or the
+                                      bound of the target lists the host was told about) */
 
 #define RELAXKV_DTYPE_F32  0
 #define RELAXKV_DTYPE_BF16 1
@@ -119,9 +136,7 @@ typedef struct relaxkv_problem {
  *   rank     [L][T_c]      rank[l*T_c + j] = rank of position j within R_l, or -1 when j is
  *                          not an active target of layer l (position-indexed view of src).
  *   counts   [L+2]         counts[0] = |U|; counts[1+l] = |R_l|; counts[L+1] = error
- *                          word: bit 0 when a NaN score reached relaxkv_select or
- *                          relaxkv_select_global, bit 1 when relaxkv_build_sets_global
- *                          got an invalid target list (cleared by relaxkv_select).
+ *                          word (RELAXKV_ERR_* bits; cleared by relaxkv_select).
  *   edges    [2L]          edges[l] = sum_{p in R_l} |C_l(p)| (App. A.2 edge count);
  *                          edges[L+l] = sum_{p in R_l} (p+1), the full-prefix count.
  *   ctx      [L][T_c]      context lists of the construction variants (first |U| entries
@@ -288,28 +303,38 @@ relaxkv_status relaxkv_build_sets_global(const relaxkv_problem* p, relaxkv_sets*
  * {j <= p} (RELAXKV_CONTEXT_FULL), where K~_j, V~_j are the fresh row of j when
  * j is in R_l and the naive cached row of j otherwise, read from KV head
  * h / (H / H_kv).
- *   q_new    device [|R_l|][H][d]     fresh queries, rows in R_l order.
- *   k_new    device [|R_l|][H_kv][d]  fresh keys, rows in R_l order.
- *   v_new    device [|R_l|][H_kv][d]  fresh values, rows in R_l order.
- *   out      device out [|R_l|][H][d] dtype: attention output before o_proj.
- *   lse_out  optional device out [|R_l|][H] float32: natural-log normaliser.
- * |R_l| is read on the device from s->counts; the host needs no count.  The
+ *   q_new    device [n_rows][H][d]     fresh queries, rows in R_l order.
+ *   k_new    device [n_rows][H_kv][d]  fresh keys, rows in R_l order.
+ *   v_new    device [n_rows][H_kv][d]  fresh values, rows in R_l order.
+ *   n_rows   rows the caller allocated in each of q_new, k_new, v_new, out and
+ *            lse_out (>= 0; normally |R_l|, which the caller learns from
+ *            relaxkv_counts_to_host or bounds by min(T_c, (L - layer) k)); the
+ *            row pointers may be NULL when n_rows is 0.
+ *   out      device out [n_rows][H][d] dtype: attention output before o_proj.
+ *   lse_out  optional device out [n_rows][H] float32: natural-log normaliser.
+ * |R_l| is read on the device from s->counts.  Targets t < min(|R_l|, n_rows)
+ * are computed; when |R_l| exceeds n_rows (or the bound of the lists s says it
+ * holds) the surplus targets are not computed and RELAXKV_ERR_ROWS is set in
+ * the error word, so no row past the caller's buffers is read or written.  The
  * naive cache of the layer is read from p->k_cache / p->v_cache.  A target
  * whose context is empty (only with relaxkv_build_sets_global, union context)
  * gets O = 0 and lse = -inf.
  */
 relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets* s,
                                    int32_t layer, const void* q_new, const void* k_new,
-                                   const void* v_new, void* out, float* lse_out,
-                                   int32_t context_mode, void* stream);
+                                   const void* v_new, int32_t n_rows, void* out,
+                                   float* lse_out, int32_t context_mode, void* stream);
 
 /*
  * Cache update of layer `layer` (Sec. 3.4 cache-update semantics; Algorithm 1,
  * cache-update step; App. A.2): the fresh K/V rows of the active targets R_l
  * overwrite the layer's cache entries at their positions; every other entry
  * keeps its value.
- *   k_new, v_new      device [|R_l|][H_kv][d] in dtype, R_l order (the rows given
+ *   k_new, v_new      device [n_rows][H_kv][d] in dtype, R_l order (the rows given
  *                     to relaxkv_sparse_attn).
+ *   n_rows            rows allocated in k_new and v_new (>= 0); as in
+ *                     relaxkv_sparse_attn, only targets t < min(|R_l|, n_rows) are
+ *                     written and RELAXKV_ERR_ROWS is set when |R_l| is larger.
  *   k_cache, v_cache  device [L][H_kv][T_c][d] in dtype: the cache to update in
  *                     place.  It may be p->k_cache / p->v_cache themselves, or an
  *                     output cache the caller initialised from them.
@@ -319,7 +344,8 @@ relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets*
  */
 relaxkv_status relaxkv_update_cache(const relaxkv_problem* p, const relaxkv_sets* s,
                                     int32_t layer, const void* k_new, const void* v_new,
-                                    void* k_cache, void* v_cache, void* stream);
+                                    int32_t n_rows, void* k_cache, void* v_cache,
+                                    void* stream);
 
 /* Host only.  Device scratch bytes relaxkv_query_attn needs (0 for float32
  * problems, which need none; 0 when p is invalid). */
@@ -354,8 +380,9 @@ relaxkv_status relaxkv_query_attn(const relaxkv_problem* p, int32_t layer, const
  * Synchronising.  Copies s->counts ([L+2] int32) to host_counts and, when
  * host_edges is not NULL, s->edges ([2L] int64) to host_edges, after all work
  * queued on `stream`.  Returns RELAXKV_EINVAL when the device error word is
- * set (a NaN score, or an invalid global target list), RELAXKV_EDEVICE on a HIP
- * error.
+ * set (RELAXKV_ERR_* bits: a NaN score, an invalid global target list, or more
+ * active targets than an attention or cache-update call could process; the
+ * counts are still copied), RELAXKV_EDEVICE on a HIP error.
  */
 relaxkv_status relaxkv_counts_to_host(const relaxkv_sets* s, int32_t* host_counts,
                                       int64_t* host_edges, void* stream);

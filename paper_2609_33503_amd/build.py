@@ -4,10 +4,18 @@ Every source under ``csrc/`` is compiled by hipcc (one process per file, in
 parallel) and linked into ``paper_2609_33503_amd/librelaxkv.so``.  All device
 code is compiled with packed-fp32 instructions disabled.
 Run as ``python -m paper_2609_33503_amd.build``.
+
+Next to the library the build writes ``librelaxkv.build.json``: a digest of
+every source and header it compiled, the build flags, and the digest of the
+library file itself.  ``relaxkv.load()`` refuses a library whose record does
+not match the sources in the tree, so a binary never runs against sources it
+was not built from.
 """
 
 from __future__ import annotations
 
+import hashlib
+import json
 import os
 import shutil
 import subprocess
@@ -19,12 +27,14 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "librelaxkv.so")
+RECORD = os.path.join(PKG, "librelaxkv.build.json")
 BUILD_DIR = os.path.join(PKG, "_build")
 ARCH = "gfx950"
 
-COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
-          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-Wno-unused-command-line-argument", f"-I{INCLUDE}", f"-I{CSRC}"]
+FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-Wno-unused-command-line-argument"]
+COMMON = FLAGS + [f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
 def _hipcc():
@@ -43,6 +53,53 @@ PER_FILE = {"attn.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-sched-strategy=ma
             "query_attn.hip": ["-fno-honor-nans"]}
 
 
+def _sources(root):
+    """Every file the library is built from, as (path relative to root, path)."""
+    out = []
+    for sub, exts in (("paper_2609_33503_amd/csrc", (".hip", ".cpp", ".h")), ("include", (".h",))):
+        d = os.path.join(root, sub)
+        for f in sorted(os.listdir(d)):
+            if f.endswith(exts):
+                out.append((f"{sub}/{f}", os.path.join(d, f)))
+    return out
+
+
+def source_digest(root=ROOT):
+    """sha256 over the sources and headers (names and bytes) and the build flags."""
+    h = hashlib.sha256()
+    for rel, path in _sources(root):
+        with open(path, "rb") as f:
+            data = f.read()
+        h.update(rel.encode() + b"\0" + str(len(data)).encode() + b"\0" + data)
+    h.update(json.dumps({"flags": FLAGS, "per_file": PER_FILE}, sort_keys=True).encode())
+    return h.hexdigest()
+
+
+def file_digest(path):
+    h = hashlib.sha256()
+    with open(path, "rb") as f:
+        for chunk in iter(lambda: f.read(1 << 20), b""):
+            h.update(chunk)
+    return h.hexdigest()
+
+
+def verify(lib_path=OUT, record_path=RECORD, root=ROOT):
+    """Raise RuntimeError unless the library at lib_path was built from the
+    sources under root (its build record matches both)."""
+    try:
+        with open(record_path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        raise RuntimeError(f"{lib_path} has no build record ({record_path}): rebuild it with "
+                           "`python -m paper_2609_33503_amd.build`") from None
+    if rec.get("library_sha256") != file_digest(lib_path):
+        raise RuntimeError(f"{lib_path} is not the library its build record describes: rebuild it")
+    if rec.get("sources_sha256") != source_digest(root):
+        raise RuntimeError(f"{lib_path} was built from other sources than the ones in the tree "
+                           "(a source, header or build flag changed since): rebuild it with "
+                           "`python -m paper_2609_33503_amd.build`")
+
+
 def _compile(src):
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
     extra = PER_FILE.get(os.path.basename(src), [])
@@ -57,6 +114,7 @@ def _compile(src):
 
 def build(verbose=False):
     os.makedirs(BUILD_DIR, exist_ok=True)
+    digest = source_digest()
     srcs = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
                   if f.endswith((".hip", ".cpp")))
     with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
@@ -67,6 +125,11 @@ def build(verbose=False):
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stderr)
     os.replace(tmp, OUT)
+    rec_tmp = RECORD + ".tmp"
+    with open(rec_tmp, "w") as f:
+        json.dump({"sources_sha256": digest, "library_sha256": file_digest(OUT),
+                   "arch": ARCH}, f, indent=1)
+    os.replace(rec_tmp, RECORD)
     if verbose:
         print("built", OUT)
     return OUT

@@ -51,9 +51,11 @@ struct AttnArgs {
     const int32_t* R_idx;
     const int32_t* R_u;
     const int32_t* counts;
+    int32_t* err;            // the error word counts[L+1]
     void* out;
     float* lse;
     int H, Hkv, G, T, layer, BT;
+    int cap;                 // rows this launch may process (row capacity, host bound)
     float scale;             // softmax scale (natural units)
 };
 
@@ -112,7 +114,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     const int Hkv = a.Hkv;
     const int g = blockIdx.x % Hkv;
     const int tile_rev = blockIdx.x / Hkv;
-    const int nR = a.counts[1 + a.layer];
+    const int nR_dev = a.counts[1 + a.layer];
+    const int nR = min(nR_dev, a.cap);
+    if (nR_dev > a.cap && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(a.err, RELAXKV_ERR_ROWS);
     const int ntiles = (nR + a.BT - 1) / a.BT;
     if (tile_rev >= ntiles) return;
     const int tile = ntiles - 1 - tile_rev;          // heaviest tiles first
@@ -376,8 +380,9 @@ __global__ __launch_bounds__(64) void attn_f32(AttnArgs a) {
     constexpr int DPL = D / 64;            // d values owned per lane
     __shared__ float qs[D];
     const int t = blockIdx.x, head = blockIdx.y;
-    const int nR = a.counts[1 + a.layer];
-    if (t >= nR) return;
+    const int nR_dev = a.counts[1 + a.layer];
+    if (nR_dev > a.cap && t == 0 && head == 0 && threadIdx.x == 0) atomicOr(a.err, RELAXKV_ERR_ROWS);
+    if (t >= min(nR_dev, a.cap)) return;
     const int lane = threadIdx.x;
     const int g = head / a.G;
     const int off = a.R_off[a.layer];
@@ -439,6 +444,7 @@ static_assert(kAttnRows == kNW * 32, "rows per workgroup");
 
 template <int D, bool FULL>
 void launch_one(const AttnArgs& a, bool bf16, int n_bound, hipStream_t st) {
+    n_bound = n_bound > 0 ? n_bound : 1;                 // workgroup 0 still checks the count
     if (bf16) {
         const int ntiles = (n_bound + a.BT - 1) / a.BT;
         hipLaunchKernelGGL((attn_bf16<D, FULL, kNW>), dim3(ntiles * a.Hkv), dim3(kNW * 64), 0, st, a);
@@ -451,7 +457,8 @@ void launch_one(const AttnArgs& a, bool bf16, int n_bound, hipStream_t st) {
 
 hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
                               const void* q_new, const void* k_new, const void* v_new,
-                              void* out, float* lse_out, int context_mode, hipStream_t st) {
+                              int n_rows, void* out, float* lse_out, int context_mode,
+                              hipStream_t st) {
     const bool bf16 = p.dtype == RELAXKV_DTYPE_BF16;
     const size_t esz = bf16 ? 2 : 4;
     const size_t layer_elems = (size_t)p.H_kv * p.T_c * p.d;
@@ -472,6 +479,7 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.R_idx = s.R_idx;
     a.R_u = s.R_u;
     a.counts = s.counts;
+    a.err = s.counts + p.L + 1;
     a.out = out;
     a.lse = lse_out;
     a.H = p.H;
@@ -481,11 +489,10 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.layer = layer;
     a.BT = bf16 ? kAttnRows / a.G : 1;
     a.scale = p.softmax_scale > 0.f ? p.softmax_scale : 1.0f / sqrtf((float)p.d);
-    // |R_l| <= |union of S_l' for l' >= l| <= min(T_c, (L - l) k) for RelaxKV's
-    // targets, <= T_c for a global target list; the device count decides which
-    // workgroups run.
-    const long kb = s.global_targets ? (long)p.T_c : (long)(p.L - layer) * s.k;
-    const int n_bound = (int)(kb < p.T_c ? kb : p.T_c);
+    // The grid covers the row cap; the device count (clamped to it) decides
+    // which workgroups run.
+    a.cap = row_cap(p, s, layer, n_rows);
+    const int n_bound = a.cap;
     const bool full = context_mode == RELAXKV_CONTEXT_FULL;
     if (p.d == 128) {
         full ? launch_one<128, true>(a, bf16, n_bound, st) : launch_one<128, false>(a, bf16, n_bound, st);

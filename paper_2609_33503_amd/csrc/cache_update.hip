@@ -4,9 +4,10 @@
 //
 // One pass of 16-byte copies: thread -> (target t, KV head g, 16-byte part), so
 // consecutive threads read consecutive bytes of the fresh rows and write whole
-// d-long rows of the cache.  |R_l| is read on the device; the grid is sized from
-// the host bound |R_l| <= min(T_c, (L - l) k) (T_c for a global target list)
-// and surplus threads exit.
+// d-long rows of the cache.  |R_l| is read on the device and clamped to the
+// launch's row cap (the caller's row capacity and the host bound on |R_l|); the
+// grid is sized from that cap and surplus threads exit.  A clamped count sets
+// RELAXKV_ERR_ROWS.
 
 #include "dev_common.h"
 #include "internal.h"
@@ -17,9 +18,11 @@ namespace {
 __global__ __launch_bounds__(256) void update_cache_rows(
     const u32x4* __restrict__ k_new, const u32x4* __restrict__ v_new, u32x4* __restrict__ k_cache,
     u32x4* __restrict__ v_cache, const int32_t* __restrict__ R_off,
-    const int32_t* __restrict__ R_idx, const int32_t* __restrict__ counts, int layer, int Hkv,
-    int T, int parts) {
-    const int nR = counts[1 + layer];
+    const int32_t* __restrict__ R_idx, const int32_t* __restrict__ counts,
+    int32_t* __restrict__ err, int layer, int Hkv, int T, int parts, int cap) {
+    const int nR_dev = counts[1 + layer];
+    const int nR = min(nR_dev, cap);
+    if (nR_dev > cap && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, RELAXKV_ERR_ROWS);
     const long n = (long)nR * Hkv * parts;
     const int32_t* pos = R_idx + R_off[layer];
     for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n;
@@ -37,19 +40,21 @@ __global__ __launch_bounds__(256) void update_cache_rows(
 }  // namespace
 
 hipError_t launch_update_cache(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
-                               const void* k_new, const void* v_new, void* k_cache,
+                               const void* k_new, const void* v_new, int n_rows, void* k_cache,
                                void* v_cache, hipStream_t st) {
     const size_t esz = p.dtype == RELAXKV_DTYPE_BF16 ? 2 : 4;
     const int parts = (int)(p.d * esz / 16);             // 16-byte parts per row
     const size_t layer_bytes = (size_t)p.H_kv * p.T_c * p.d * esz;
     u32x4* kc = (u32x4*)((char*)k_cache + (size_t)layer * layer_bytes);
     u32x4* vc = (u32x4*)((char*)v_cache + (size_t)layer * layer_bytes);
-    const long kb = s.global_targets ? (long)p.T_c : (long)(p.L - layer) * s.k;
-    const long n_bound = (kb < p.T_c ? kb : p.T_c) * (long)p.H_kv * parts;
-    const long blocks = (n_bound + 255) / 256;
+    const int cap = row_cap(p, s, layer, n_rows);
+    const long n_bound = (long)cap * p.H_kv * parts;
+    long blocks = (n_bound + 255) / 256;
+    if (blocks < 1) blocks = 1;                          // block 0 still checks the count
     hipLaunchKernelGGL(update_cache_rows, dim3((unsigned)(blocks < 8192 ? blocks : 8192)),
                        dim3(256), 0, st, (const u32x4*)k_new, (const u32x4*)v_new, kc, vc,
-                       s.R_off, s.R_idx, s.counts, layer, p.H_kv, p.T_c, parts);
+                       s.R_off, s.R_idx, s.counts, s.counts + p.L + 1, layer, p.H_kv, p.T_c,
+                       parts, cap);
     return hipGetLastError();
 }
 

@@ -57,14 +57,27 @@ hipError_t launch_build_sets_global(const relaxkv_problem& p, const relaxkv_sets
 hipError_t launch_build_sets(const relaxkv_problem& p, const relaxkv_sets& s,
                              hipStream_t st);
 hipError_t launch_update_cache(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
-                               const void* k_new, const void* v_new, void* k_cache,
+                               const void* k_new, const void* v_new, int n_rows, void* k_cache,
                                void* v_cache, hipStream_t st);
 hipError_t launch_query_attn(const relaxkv_problem& p, int layer, const void* k_cache,
                              const void* v_cache, const void* k_q, const void* v_q, void* out,
                              float* lse_out, char* ws, hipStream_t st);
 hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, int layer,
                               const void* q_new, const void* k_new, const void* v_new,
-                              void* out, float* lse_out, int context_mode, hipStream_t st);
+                              int n_rows, void* out, float* lse_out, int context_mode,
+                              hipStream_t st);
+
+// Rows an attention or cache-update launch may process for layer `layer`: the
+// caller's row capacity, and the bound on |R_l| of the lists the sets hold
+// (min(T_c, (L - l) k) for RelaxKV's targets: R_l lies in the union of S_l'
+// for l' >= l; T_c for a global target list).  Kernels clamp the device count
+// to it and set RELAXKV_ERR_ROWS when they have to.
+inline int row_cap(const relaxkv_problem& p, const relaxkv_sets& s, int layer, int n_rows) {
+    const long kb = s.global_targets ? (long)p.T_c : (long)(p.L - layer) * s.k;
+    long cap = kb < p.T_c ? kb : p.T_c;
+    if (n_rows < cap) cap = n_rows;
+    return (int)cap;
+}
 
 
 }  // namespace relaxkv

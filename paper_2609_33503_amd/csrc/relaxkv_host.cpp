@@ -214,28 +214,29 @@ relaxkv_status relaxkv_build_sets_global(const relaxkv_problem* p, relaxkv_sets*
 
 relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets* s,
                                    int32_t layer, const void* q_new, const void* k_new,
-                                   const void* v_new, void* out, float* lse_out,
-                                   int32_t context_mode, void* stream) {
+                                   const void* v_new, int32_t n_rows, void* out,
+                                   float* lse_out, int32_t context_mode, void* stream) {
     relaxkv_status st = relaxkv_validate(p);
     if (st != RELAXKV_OK) return st;
     if (!sets_match(p, s)) return RELAXKV_EINVAL;
-    if (layer < 0 || layer >= p->L) return RELAXKV_EINVAL;
-    if (!q_new || !k_new || !v_new || !out) return RELAXKV_EINVAL;
+    if (layer < 0 || layer >= p->L || n_rows < 0) return RELAXKV_EINVAL;
+    if (n_rows > 0 && (!q_new || !k_new || !v_new || !out)) return RELAXKV_EINVAL;
     if (context_mode != RELAXKV_CONTEXT_UNION && context_mode != RELAXKV_CONTEXT_FULL)
         return RELAXKV_EINVAL;
-    return from_hip(launch_sparse_attn(*p, *s, layer, q_new, k_new, v_new, out, lse_out,
-                                       context_mode, (hipStream_t)stream));
+    return from_hip(launch_sparse_attn(*p, *s, layer, q_new, k_new, v_new, n_rows, out,
+                                       lse_out, context_mode, (hipStream_t)stream));
 }
 
 relaxkv_status relaxkv_update_cache(const relaxkv_problem* p, const relaxkv_sets* s,
                                     int32_t layer, const void* k_new, const void* v_new,
-                                    void* k_cache, void* v_cache, void* stream) {
+                                    int32_t n_rows, void* k_cache, void* v_cache,
+                                    void* stream) {
     relaxkv_status st = relaxkv_validate(p);
     if (st != RELAXKV_OK) return st;
     if (!sets_match(p, s)) return RELAXKV_EINVAL;
-    if (layer < 0 || layer >= p->L) return RELAXKV_EINVAL;
-    if (!k_new || !v_new || !k_cache || !v_cache) return RELAXKV_EINVAL;
-    return from_hip(launch_update_cache(*p, *s, layer, k_new, v_new, k_cache, v_cache,
+    if (layer < 0 || layer >= p->L || n_rows < 0) return RELAXKV_EINVAL;
+    if ((n_rows > 0 && (!k_new || !v_new)) || !k_cache || !v_cache) return RELAXKV_EINVAL;
+    return from_hip(launch_update_cache(*p, *s, layer, k_new, v_new, n_rows, k_cache, v_cache,
                                         (hipStream_t)stream));
 }
 

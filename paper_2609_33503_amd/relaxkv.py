@@ -18,6 +18,7 @@ import torch
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librelaxkv.so")
 
 OK, EINVAL, ENOSPACE, EUNSUPPORTED, EDEVICE = 0, -1, -2, -3, -4
+ERR_NAN_SCORE, ERR_BAD_TARGETS, ERR_ROWS = 1, 2, 4      # bits of the device error word
 DTYPE_F32, DTYPE_BF16 = 0, 1
 CONTEXT_UNION, CONTEXT_FULL = 0, 1
 CONTEXT_SETS_UNION, CONTEXT_SETS_GLOBAL, CONTEXT_SETS_LAYERWISE = 0, 1, 2
@@ -57,13 +58,18 @@ _lib = None
 
 
 def load(path=None):
-    """Load the library (once).  Raises if it has not been built."""
+    """Load the library (once).  Raises if it has not been built, or if the
+    in-tree library was not built from the sources in the tree (its build
+    record, written by ``build.py``, must match them)."""
     global _lib
     if _lib is not None:
         return _lib
     p = path or _LIB_PATH
     if not os.path.exists(p):
         raise RuntimeError(f"{p} is missing: build it with `python -m paper_2609_33503_amd.build`")
+    if path is None:
+        from . import build
+        build.verify(p)
     lib = ctypes.CDLL(p)
     lib.relaxkv_status_string.restype = c_char_p
     lib.relaxkv_status_string.argtypes = [c_int32]
@@ -94,11 +100,11 @@ def load(path=None):
                                               c_void_p]
     lib.relaxkv_sparse_attn.restype = c_int32
     lib.relaxkv_sparse_attn.argtypes = [POINTER(Problem), POINTER(Sets), c_int32, c_void_p,
-                                        c_void_p, c_void_p, c_void_p, c_void_p, c_int32,
-                                        c_void_p]
+                                        c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
+                                        c_int32, c_void_p]
     lib.relaxkv_update_cache.restype = c_int32
     lib.relaxkv_update_cache.argtypes = [POINTER(Problem), POINTER(Sets), c_int32, c_void_p,
-                                         c_void_p, c_void_p, c_void_p, c_void_p]
+                                         c_void_p, c_int32, c_void_p, c_void_p, c_void_p]
     lib.relaxkv_query_attn_workspace_bytes.restype = c_size_t
     lib.relaxkv_query_attn_workspace_bytes.argtypes = [POINTER(Problem)]
     lib.relaxkv_query_attn.restype = c_int32
@@ -133,6 +139,29 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _need(t, name, dtype, shape, device):
+    """Raise ValueError unless t is a contiguous tensor on `device` with this dtype
+    and shape (None in `shape` matches any size).  Every pointer the library
+    gets passes through here, so a host tensor, a tensor on another device or
+    one too small never reaches a kernel."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the problem's tensors are on {device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.dim() != len(shape) or any(want is not None and got != want
+                                    for got, want in zip(t.shape, shape)):
+        want = tuple("*" if x is None else x for x in shape)
+        raise ValueError(f"{name} must have shape {want}, got {tuple(t.shape)}")
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
 def anchor_count(ratio, T_c):
     k = load().relaxkv_anchor_count(float(ratio), int(T_c))
     _check(OK if k > 0 else k, "relaxkv_anchor_count")
@@ -150,20 +179,21 @@ class Request:
 
     def __init__(self, q, k_cache, v_cache, anchor_ratio, softmax_scale=0.0, q_lse=None):
         lib = load()
-        for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache)):
-            if not t.is_cuda or not t.is_contiguous():
-                raise ValueError(f"{name} must be a contiguous device tensor")
-        if q.dtype != k_cache.dtype or v_cache.dtype != k_cache.dtype:
-            raise ValueError("q, k_cache and v_cache must share a dtype")
-        if q_lse is not None and (q_lse.dtype != torch.float32 or not q_lse.is_contiguous()):
-            raise ValueError("q_lse must be contiguous float32")
-        L, Qn, H, d = q.shape
-        _, H_kv, T_c, d2 = k_cache.shape
-        if k_cache.shape[0] != L or d2 != d or tuple(v_cache.shape) != tuple(k_cache.shape):
-            raise ValueError("inconsistent shapes")
+        if not isinstance(q, torch.Tensor) or not q.is_cuda or q.dim() != 4:
+            raise ValueError("q must be a [L][n_query][H][d] device tensor")
         dt = {torch.bfloat16: DTYPE_BF16, torch.float32: DTYPE_F32}.get(q.dtype)
         if dt is None:
             raise ValueError("dtype must be bfloat16 or float32")
+        L, Qn, H, d = q.shape
+        if not isinstance(k_cache, torch.Tensor) or k_cache.dim() != 4:
+            raise ValueError("k_cache must be a [L][H_kv][T_c][d] tensor")
+        H_kv, T_c = k_cache.shape[1], k_cache.shape[2]
+        self.device = q.device
+        _need(q, "q", q.dtype, (L, Qn, H, d), self.device)
+        _need(k_cache, "k_cache", q.dtype, (L, H_kv, T_c, d), self.device)
+        _need(v_cache, "v_cache", q.dtype, (L, H_kv, T_c, d), self.device)
+        if q_lse is not None:
+            _need(q_lse, "q_lse", torch.float32, (L, Qn, H), self.device)
         self.dtype = q.dtype
         self.tensors = (q, k_cache, v_cache, q_lse)
         self.p = Problem(L, T_c, Qn, H, H_kv, d, dt, float(softmax_scale), float(anchor_ratio),
@@ -180,13 +210,25 @@ class Request:
         return load().relaxkv_sets_bytes(ctypes.byref(self.p))
 
     def alloc_workspace(self):
-        return torch.empty(self.workspace_bytes(), dtype=torch.uint8,
-                           device=self.tensors[1].device)
+        return torch.empty(self.workspace_bytes(), dtype=torch.uint8, device=self.device)
+
+    # ---- argument checks shared by the calls
+    def _scores(self, scores):
+        _need(scores, "scores", torch.float32, (self.L, self.T_c), self.device)
+
+    def _sets(self, sets):
+        if not isinstance(sets, SetsBuffer) or sets.buf.device != self.device or \
+                (sets.s.L, sets.s.T_c, sets.s.k) != (self.L, self.T_c, self.k):
+            raise ValueError("sets must come from alloc_sets() of a request of this shape")
+
+    def _ws(self, ws, name="ws"):
+        if not isinstance(ws, torch.Tensor) or ws.device != self.device or not ws.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous tensor on {self.device}")
 
     def alloc_sets(self):
         """A device buffer for the sets and its bound descriptor."""
         nbytes = self.sets_bytes()
-        buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.tensors[1].device)
+        buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
         base = buf.data_ptr()
         pad = (-base) % 256
         s = Sets()
@@ -196,20 +238,27 @@ class Request:
 
     # ---- the four calls
     def score(self, ws, scores, stream=None):
-        _check(load().relaxkv_score(ctypes.byref(self.p), _ptr(ws), ws.numel(), _ptr(scores),
+        self._ws(ws)
+        self._scores(scores)
+        _check(load().relaxkv_score(ctypes.byref(self.p), _ptr(ws), _nbytes(ws), _ptr(scores),
                                     _stream(stream)), "relaxkv_score")
 
     def select(self, scores, sets, stream=None):
+        self._scores(scores)
+        self._sets(sets)
         _check(load().relaxkv_select(ctypes.byref(self.p), _ptr(scores), ctypes.byref(sets.s),
                                      _stream(stream)), "relaxkv_select")
 
     def build_sets(self, sets, stream=None):
+        self._sets(sets)
         _check(load().relaxkv_build_sets(ctypes.byref(self.p), ctypes.byref(sets.s),
                                          _stream(stream)), "relaxkv_build_sets")
 
     def build_sets_context(self, scores, construction, sets, stream=None):
         """RelaxKV's anchors and targets with the context set replaced
         (CONTEXT_SETS_UNION / _GLOBAL / _LAYERWISE); scores [L][T_c] f32."""
+        self._scores(scores)
+        self._sets(sets)
         _check(load().relaxkv_build_sets_context(ctypes.byref(self.p), _ptr(scores),
                                                  int(construction), ctypes.byref(sets.s),
                                                  _stream(stream)), "relaxkv_build_sets_context")
@@ -217,46 +266,58 @@ class Request:
     # ---- matched-target variants: one global target list for every layer
     def select_global(self, scores, target_ratio, sets, g, targets, n_targets, stream=None):
         """g [T_c] f32, targets [T_c] int32 and n_targets [1] int32 are outputs."""
-        for t, dt, n in ((g, torch.float32, self.T_c), (targets, torch.int32, self.T_c),
-                         (n_targets, torch.int32, 1)):
-            if t.dtype != dt or not t.is_contiguous() or t.numel() < n:
-                raise ValueError("select_global outputs: g f32 [T_c], targets int32 [T_c], "
-                                 "n_targets int32 [1]")
+        self._scores(scores)
+        self._sets(sets)
+        _need(g, "g", torch.float32, (self.T_c,), self.device)
+        _need(targets, "targets", torch.int32, (self.T_c,), self.device)
+        _need(n_targets, "n_targets", torch.int32, (1,), self.device)
         _check(load().relaxkv_select_global(ctypes.byref(self.p), _ptr(scores),
                                             float(target_ratio), ctypes.byref(sets.s), _ptr(g),
                                             _ptr(targets), _ptr(n_targets), _stream(stream)),
                "relaxkv_select_global")
 
     def build_sets_global(self, sets, targets, n_targets, stream=None):
-        """targets: int32 device, ascending; n_targets: int32 device [1]."""
-        for t in (targets, n_targets):
-            if t.dtype != torch.int32 or not t.is_contiguous() or not t.is_cuda:
-                raise ValueError("targets and n_targets must be contiguous int32 device tensors")
+        """targets: int32 device [T_c], ascending in its first n_targets entries;
+        n_targets: int32 device [1]."""
+        self._sets(sets)
+        _need(targets, "targets", torch.int32, (self.T_c,), self.device)
+        _need(n_targets, "n_targets", torch.int32, (1,), self.device)
         _check(load().relaxkv_build_sets_global(ctypes.byref(self.p), ctypes.byref(sets.s),
                                                 _ptr(targets), _ptr(n_targets), _stream(stream)),
                "relaxkv_build_sets_global")
 
     def sparse_attn(self, sets, layer, q_new, k_new, v_new, out, lse_out=None,
                     context_mode=CONTEXT_UNION, stream=None):
-        for t in (q_new, k_new, v_new, out):
-            if not t.is_contiguous() or t.dtype != self.dtype:
-                raise ValueError("fresh rows and out must be contiguous, in the problem dtype")
+        """q_new/out [n][H][d], k_new/v_new [n][H_kv][d], lse_out [n][H] f32, with n
+        rows allocated (normally |R_l|; targets past n are not computed and set the
+        device error word)."""
+        self._sets(sets)
+        n = q_new.shape[0] if isinstance(q_new, torch.Tensor) and q_new.dim() == 3 else -1
+        _need(q_new, "q_new", self.dtype, (n, self.H, self.d), self.device)
+        _need(k_new, "k_new", self.dtype, (n, self.H_kv, self.d), self.device)
+        _need(v_new, "v_new", self.dtype, (n, self.H_kv, self.d), self.device)
+        _need(out, "out", self.dtype, (n, self.H, self.d), self.device)
+        if lse_out is not None:
+            _need(lse_out, "lse_out", torch.float32, (n, self.H), self.device)
         _check(load().relaxkv_sparse_attn(ctypes.byref(self.p), ctypes.byref(sets.s), int(layer),
-                                          _ptr(q_new), _ptr(k_new), _ptr(v_new), _ptr(out),
-                                          _ptr(lse_out), int(context_mode), _stream(stream)),
+                                          _ptr(q_new), _ptr(k_new), _ptr(v_new), int(n),
+                                          _ptr(out), _ptr(lse_out), int(context_mode),
+                                          _stream(stream)),
                "relaxkv_sparse_attn")
 
 
     def update_cache(self, sets, layer, k_new, v_new, k_cache, v_cache, stream=None):
-        """Fresh rows of R_l into the cache (k_cache/v_cache: [L][H_kv][T_c][d])."""
-        for t in (k_new, v_new, k_cache, v_cache):
-            if not t.is_contiguous() or t.dtype != self.dtype:
-                raise ValueError("rows and caches must be contiguous, in the problem dtype")
-        if tuple(k_cache.shape) != tuple(self.tensors[1].shape) or \
-                tuple(v_cache.shape) != tuple(self.tensors[2].shape):
-            raise ValueError("caches must have the problem's cache shape")
+        """Fresh rows of R_l (k_new/v_new [n][H_kv][d]) into the cache
+        (k_cache/v_cache: [L][H_kv][T_c][d])."""
+        self._sets(sets)
+        n = k_new.shape[0] if isinstance(k_new, torch.Tensor) and k_new.dim() == 3 else -1
+        _need(k_new, "k_new", self.dtype, (n, self.H_kv, self.d), self.device)
+        _need(v_new, "v_new", self.dtype, (n, self.H_kv, self.d), self.device)
+        cache = (self.L, self.H_kv, self.T_c, self.d)
+        _need(k_cache, "k_cache", self.dtype, cache, self.device)
+        _need(v_cache, "v_cache", self.dtype, cache, self.device)
         _check(load().relaxkv_update_cache(ctypes.byref(self.p), ctypes.byref(sets.s), int(layer),
-                                           _ptr(k_new), _ptr(v_new), _ptr(k_cache),
+                                           _ptr(k_new), _ptr(v_new), int(n), _ptr(k_cache),
                                            _ptr(v_cache), _stream(stream)),
                "relaxkv_update_cache")
 
@@ -267,18 +328,25 @@ class Request:
 
     def alloc_query_workspace(self):
         n = self.query_attn_workspace_bytes()
-        return None if n == 0 else torch.empty(n, dtype=torch.uint8, device=self.tensors[1].device)
+        return None if n == 0 else torch.empty(n, dtype=torch.uint8, device=self.device)
 
     def query_attn(self, layer, k_cache, v_cache, k_q, v_q, out, lse_out=None, ws=None,
                    stream=None):
-        """k_cache/v_cache [L][H_kv][T_c][d]; k_q/v_q [n_query][H_kv][d]; out [n_query][H][d]."""
-        for t in (k_cache, v_cache, k_q, v_q, out):
-            if not t.is_contiguous() or t.dtype != self.dtype:
-                raise ValueError("caches, query keys/values and out must be contiguous, "
-                                 "in the problem dtype")
+        """k_cache/v_cache [L][H_kv][T_c][d]; k_q/v_q [n_query][H_kv][d]; out [n_query][H][d];
+        lse_out [n_query][H] f32."""
+        cache = (self.L, self.H_kv, self.T_c, self.d)
+        _need(k_cache, "k_cache", self.dtype, cache, self.device)
+        _need(v_cache, "v_cache", self.dtype, cache, self.device)
+        _need(k_q, "k_q", self.dtype, (self.n_query, self.H_kv, self.d), self.device)
+        _need(v_q, "v_q", self.dtype, (self.n_query, self.H_kv, self.d), self.device)
+        _need(out, "out", self.dtype, (self.n_query, self.H, self.d), self.device)
+        if lse_out is not None:
+            _need(lse_out, "lse_out", torch.float32, (self.n_query, self.H), self.device)
+        if ws is not None:
+            self._ws(ws)
         _check(load().relaxkv_query_attn(ctypes.byref(self.p), int(layer), _ptr(k_cache),
                                          _ptr(v_cache), _ptr(k_q), _ptr(v_q), _ptr(out),
-                                         _ptr(lse_out), _ptr(ws), 0 if ws is None else ws.numel(),
+                                         _ptr(lse_out), _ptr(ws), 0 if ws is None else _nbytes(ws),
                                          _stream(stream)), "relaxkv_query_attn")
 
 
@@ -309,13 +377,16 @@ class SetsBuffer:
         self.ctx = view(s.ctx, L * T, torch.int32).view(L, T)
         self.g = view(s.g, T, torch.float32)
 
-    def counts_to_host(self, stream=None):
-        """(counts [L+2], edges [2L]) on the host; synchronises the stream."""
+    def counts_to_host(self, stream=None, check=True):
+        """(counts [L+2], edges [2L]) on the host; synchronises the stream.  With
+        check=True a set device error word (counts[L+1], ERR_* bits) raises
+        RelaxKVError; with check=False the counts are returned as they are."""
         L = self.req.L
         c = (c_int32 * (L + 2))()
         e = (c_int64 * (2 * L))()
         st = load().relaxkv_counts_to_host(ctypes.byref(self.s), c, e, _stream(stream))
-        _check(st, "relaxkv_counts_to_host")
+        if check or st not in (OK, EINVAL):
+            _check(st, "relaxkv_counts_to_host")
         return list(c), list(e)
 
 

@@ -18,6 +18,24 @@ def fp_tol(w):
     return ("abs", 2e-2) if w.dtype == "bf16" else ("rel", 1e-5)
 
 
+def assert_rows_close(got, ref, what, gate=1e-2, floor=1e-6):
+    """Per-row gate for bf16 attention outputs [n][H][d]: every (target, head)
+    row satisfies max_e |O - O_ref| <= gate * max_e |O_ref| + floor, so an error
+    confined to rows with small outputs (long contexts) cannot hide behind the
+    largest row of the tensor."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    if not got.size:
+        return 0.0
+    err = np.max(np.abs(got - ref), axis=-1)
+    bound = gate * np.max(np.abs(ref), axis=-1) + floor
+    worst = np.unravel_index(int(np.argmax(err / bound)), err.shape)
+    assert np.all(err <= bound), (f"{what}: row {worst} error {err[worst]:.3e} > "
+                                  f"{bound[worst]:.3e} ({gate} of its largest |O_ref| + {floor})")
+    return float(np.max(err / bound))
+
+
 def assert_close(got, ref, w, what, rel_gate=None):
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
@@ -32,6 +50,8 @@ def assert_close(got, ref, w, what, rel_gate=None):
         assert err <= tol * max(scale, 1e-30), f"{what}: rel {err / max(scale, 1e-30):.3e} > {tol}"
     if rel_gate is not None and scale > 0:
         assert err / scale <= rel_gate, f"{what}: normalised {err / scale:.3e} > {rel_gate}"
+        if got.ndim == 3:                            # attention outputs: also row by row
+            assert_rows_close(got, ref, what, gate=rel_gate)
     return err, scale
 
 

@@ -303,3 +303,62 @@ def test_update_cache_bit_exact(gpu_lib, name):
     case.req.update_cache(case.sets, 0, kn, vn, case.kc, case.vc)
     torch.cuda.synchronize()
     assert torch.equal(case.kc[1:], k_before[1:])
+
+
+@pytest.mark.parametrize("name", ["qwen-planted", "tiny"])
+def test_row_capacity_clamps_and_reports(gpu_lib, name):
+    """A row capacity below |R_l| (a caller that sized its buffers from a stale
+    count): the attention computes exactly the first n_rows targets, writes
+    nothing past them, and the device error word reports RELAXKV_ERR_ROWS, so
+    relaxkv_counts_to_host returns RELAXKV_EINVAL; the cache update writes only
+    the first n_rows rows.  The error word clears at the next selection."""
+    w = SMALL[name]
+    case = Case(w)
+    a = synthetic_scores(case.L, case.T, seed=19)
+    anchors_ref = oracle.select(a.astype(np.float64), case.k)
+    sets_ref = oracle.build_sets(anchors_ref, case.T)
+    case.req.select(torch.from_numpy(a).cuda(), case.sets)
+    compare_sets(case.gpu_sets(), sets_ref)
+    l = 1
+    R_l = sets_ref.R[l]
+    n = len(R_l)
+    m = n - 37
+    assert m > 0
+    fresh = case.fresh(l, R_l)
+    cut = tuple(t[:m].contiguous() for t in fresh)
+    sentinel = 7.0
+    out_big = torch.full((n, w.H, w.d), sentinel, dtype=case.q.dtype, device="cuda")
+    lse_big = torch.full((n, w.H), sentinel, dtype=torch.float32, device="cuda")
+    for mode, cm in (("union", relaxkv.CONTEXT_UNION), ("full", relaxkv.CONTEXT_FULL)):
+        out_big.fill_(sentinel)
+        lse_big.fill_(sentinel)
+        case.req.sparse_attn(case.sets, l, *cut, out_big[:m], lse_big[:m], context_mode=cm)
+        torch.cuda.synchronize()
+        assert bool((out_big[m:] == sentinel).all()) and bool((lse_big[m:] == sentinel).all())
+        counts, _ = case.sets.counts_to_host(check=False)
+        assert counts[case.L + 1] & relaxkv.ERR_ROWS
+        with pytest.raises(relaxkv.RelaxKVError) as e:
+            case.sets.counts_to_host()
+        assert e.value.status == relaxkv.EINVAL
+        ts = sorted({0, m // 2, m - 1})
+        O_ref, lse_ref = case.oracle_attn(l, sets_ref, fresh, mode=mode, targets=ts)
+        assert_close(out_big[ts].float().cpu().numpy(), O_ref, w, f"O {mode} clamped",
+                     rel_gate=1e-2 if w.dtype == "bf16" else None)
+        assert_close(lse_big[ts].cpu().numpy(), lse_ref, w, f"lse {mode} clamped")
+    # the cache update with the same short rows writes the first m rows only
+    k_out, v_out = case.kc.clone(), case.vc.clone()
+    case.req.update_cache(case.sets, l, cut[1], cut[2], k_out, v_out)
+    torch.cuda.synchronize()
+    short = oracle.Sets(**{**sets_ref.__dict__, "R": [r[:m] if i == l else r
+                                                      for i, r in enumerate(sets_ref.R)]})
+    kr, vr = oracle.update_cache(l, short, synth.to_f64(cut[1]), synth.to_f64(cut[2]),
+                                 synth.to_f64(case.kc[l]), synth.to_f64(case.vc[l]))
+    assert np.array_equal(synth.to_f64(k_out[l]), kr)
+    assert np.array_equal(synth.to_f64(v_out[l]), vr)
+    # the next selection clears the word; full-capacity calls then report nothing
+    case.req.select(torch.from_numpy(a).cuda(), case.sets)
+    case.req.build_sets(case.sets)
+    out, lse = case.gpu_attn(l, fresh, n)
+    case.req.update_cache(case.sets, l, fresh[1], fresh[2], k_out, v_out)
+    counts, _ = case.sets.counts_to_host()
+    assert counts[case.L + 1] == 0

@@ -20,7 +20,9 @@ HEADER = os.path.join(ROOT, "include", "relaxkv.h")
 @pytest.fixture(scope="module")
 def rk():
     from paper_2609_33503_amd import build, relaxkv
-    if not os.path.exists(relaxkv._LIB_PATH):
+    try:
+        build.verify()
+    except RuntimeError:                             # missing or stale: build it (CPU only)
         build.build()
     relaxkv.load()
     return relaxkv
@@ -165,25 +167,29 @@ def test_compute_calls_reject_before_launch(rk):
     s2 = _bound_sets(rk, p)
     s2.src = None
     assert lib.relaxkv_build_sets(ctypes.byref(p), ctypes.byref(s2), None) == rk.EINVAL
-    # sparse_attn
-    args = (fake, fake, fake, fake, None)
+    # sparse_attn: (q_new, k_new, v_new, n_rows, out, lse_out, context_mode, stream)
+    args = (fake, fake, fake, 100, fake, None)
     for layer in (-1, 4):
         assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s), layer, *args, 0,
                                        None) == rk.EINVAL
     assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s), 0, *args, 2,
                                    None) == rk.EINVAL
-    assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s), 0, None, fake, fake, fake,
-                                   None, 0, None) == rk.EINVAL
+    assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s), 0, None, fake, fake, 100,
+                                   fake, None, 0, None) == rk.EINVAL
+    assert lib.relaxkv_sparse_attn(ctypes.byref(p), ctypes.byref(s), 0, fake, fake, fake, -1,
+                                   fake, None, 0, None) == rk.EINVAL
     assert lib.relaxkv_sparse_attn(ctypes.byref(_problem(rk, d=96)), ctypes.byref(s), 0, *args,
                                    0, None) == rk.EUNSUPPORTED
-    # update_cache
+    # update_cache: (k_new, v_new, n_rows, k_cache, v_cache, stream)
     for layer in (-1, 4):
-        assert lib.relaxkv_update_cache(ctypes.byref(p), ctypes.byref(s), layer, fake, fake, fake,
-                                        fake, None) == rk.EINVAL
-    assert lib.relaxkv_update_cache(ctypes.byref(p), ctypes.byref(s), 0, fake, fake, None, fake,
-                                    None) == rk.EINVAL
-    assert lib.relaxkv_update_cache(ctypes.byref(other), ctypes.byref(s), 0, fake, fake, fake,
+        assert lib.relaxkv_update_cache(ctypes.byref(p), ctypes.byref(s), layer, fake, fake, 100,
+                                        fake, fake, None) == rk.EINVAL
+    assert lib.relaxkv_update_cache(ctypes.byref(p), ctypes.byref(s), 0, fake, fake, 100, None,
                                     fake, None) == rk.EINVAL
+    assert lib.relaxkv_update_cache(ctypes.byref(p), ctypes.byref(s), 0, fake, fake, -1, fake,
+                                    fake, None) == rk.EINVAL
+    assert lib.relaxkv_update_cache(ctypes.byref(other), ctypes.byref(s), 0, fake, fake, 100,
+                                    fake, fake, None) == rk.EINVAL
     # select_global / build_sets_global (matched-target variants)
     sg = lib.relaxkv_select_global
     for r in (-0.1, 1.5, float("nan"), float("inf")):
@@ -247,3 +253,62 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU only" in r.stderr
+
+
+def test_library_refused_when_sources_change(tmp_path):
+    """The build record ties the library to its sources: a touched source, a
+    touched header or a swapped library makes verification (and so
+    relaxkv.load()) fail."""
+    import shutil
+
+    from paper_2609_33503_amd import build
+    for sub in ("paper_2609_33503_amd/csrc", "include"):
+        shutil.copytree(os.path.join(ROOT, sub), tmp_path / sub)
+    lib = tmp_path / "librelaxkv.so"
+    lib.write_bytes(b"stand-in library bytes")
+    rec = tmp_path / "librelaxkv.build.json"
+    import json
+    rec.write_text(json.dumps({"sources_sha256": build.source_digest(str(tmp_path)),
+                               "library_sha256": build.file_digest(str(lib))}))
+    build.verify(str(lib), str(rec), str(tmp_path))            # matching record: accepted
+    src = tmp_path / "paper_2609_33503_amd/csrc/attn.hip"
+    src.write_text(src.read_text() + "\n// touched\n")
+    with pytest.raises(RuntimeError, match="other sources"):
+        build.verify(str(lib), str(rec), str(tmp_path))
+    src.write_text(src.read_text()[:-len("\n// touched\n")])
+    build.verify(str(lib), str(rec), str(tmp_path))
+    hdr = tmp_path / "include/relaxkv.h"
+    hdr.write_text(hdr.read_text() + " ")
+    with pytest.raises(RuntimeError, match="other sources"):
+        build.verify(str(lib), str(rec), str(tmp_path))
+    hdr.write_text(hdr.read_text()[:-1])
+    lib.write_bytes(b"another library")
+    with pytest.raises(RuntimeError, match="not the library"):
+        build.verify(str(lib), str(rec), str(tmp_path))
+    rec.unlink()
+    with pytest.raises(RuntimeError, match="no build record"):
+        build.verify(str(lib), str(rec), str(tmp_path))
+
+
+def test_binding_checks_tensors_before_any_call(rk):
+    """The binding's tensor checks (device, dtype, contiguity, shape) run before
+    a pointer reaches the library; here on CPU tensors, so nothing is called."""
+    import torch
+    cpu = torch.device("cpu")
+    t = torch.zeros(4, 8, 16, dtype=torch.bfloat16)
+    rk._need(t, "x", torch.bfloat16, (4, 8, 16), cpu)
+    rk._need(t, "x", torch.bfloat16, (None, 8, 16), cpu)
+    for args, msg in [((torch.float32, (4, 8, 16), cpu), "must be torch.float32"),
+                      ((torch.bfloat16, (4, 8, 17), cpu), "shape"),
+                      ((torch.bfloat16, (4, 8), cpu), "shape"),
+                      ((torch.bfloat16, (4, 8, 16), torch.device("cuda", 0)), "is on cpu")]:
+        with pytest.raises(ValueError, match=msg):
+            rk._need(t, "x", *args)
+    with pytest.raises(ValueError, match="contiguous"):
+        rk._need(t.transpose(0, 1), "x", torch.bfloat16, (8, 4, 16), cpu)
+    with pytest.raises(ValueError, match="tensor"):
+        rk._need(None, "x", torch.bfloat16, (4, 8, 16), cpu)
+    q = torch.zeros(2, 4, 8, 64, dtype=torch.bfloat16)
+    kc = torch.zeros(2, 2, 32, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="device tensor"):
+        rk.Request(q, kc, kc.clone(), 0.15)
