@@ -10,15 +10,26 @@ Reported value: repair-attention TFLOP/s = 4 H d (sum over layers of the
 unmasked causal edges sum_{p in R_l} |C_l(p)|) / step time, with the step time
 including scoring, selection and set construction.  ms_per_step / L is the
 per-layer time.  The "roofline" object covers the dominant kernel
-(sparse-context attention), timed with HIP events on the launch stream; the
-"cpu_baseline" object times the float64 oracle on a bounded sample of the same
-workload on this host's cores; the "control" object times the Full-Prefix
-Control on the same targets and reports how far its outputs are from the
-union-restricted ones, and "latent_union" repeats union and full prefix on
-inputs whose layers share a per-position latent (union about 63% of T_c).
+(sparse-context attention), timed with HIP events on the launch stream, with
+its fraction of the published bf16 peak and of the rate a plain bf16 GEMM
+reaches in the same process ("measured_peaks": a device copy and a GEMM).
+Other objects:
+- "scoring": both scoring modes, and the one-pass chain in which the
+  library's query-side completion produces the row LSE the scorer takes;
+- "control": the Full-Prefix Control on the same targets (time ratio, output
+  difference), for 512-token chunks and again for 2048-token chunks after
+  checking that those inputs are identical;
+- "latent_union": union and full prefix on inputs whose layers share a
+  per-position latent (union about 63% of T_c);
+- "workloads": the 8K Llama-shaped and the 16K Qwen-shaped workloads (anchor
+  ratios 0.05 / 0.15 / 0.30) with their set statistics;
+- "anchor_jaccard_gpu_vs_oracle_scores": anchors from the library's scores
+  against anchors from the oracle's float64 scores on sampled layers;
+- "cpu_baseline": the float64 oracle, stage by stage, on this host's cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--no-control] [--no-matched-targets] [--no-cpu-baseline]
+                       [--no-workloads]
 """
 
 from __future__ import annotations
@@ -357,16 +368,17 @@ def measured_peaks():
             "note": "2 GiB device copy (read + write bytes) and a 8192^3 bf16 torch GEMM"}
 
 
-def _input_digest(t):
+def _input_digest(t, chunk=1 << 26):
     """Device-side fingerprint of a tensor's bits (for identity checks of
     inputs that should be equal): a position-weighted sum of the bit patterns,
-    taken slice by slice along the first dimension."""
-    total = 0
-    for i, x in enumerate(t.reshape(t.shape[0], -1) if t.dim() > 1 else t.reshape(1, -1)):
-        bits = x.contiguous().view(torch.int16 if t.element_size() == 2 else torch.int32).long()
-        idx = torch.arange(bits.numel(), device=bits.device, dtype=torch.int64)
-        total += (i + 1) * int(((bits + 40503) * (idx % 65521 + 1)).sum().item())
-    return total
+    in flat chunks of at most `chunk` elements."""
+    flat = t.contiguous().view(torch.int16 if t.element_size() == 2 else torch.int32).reshape(-1)
+    total = torch.zeros((), dtype=torch.int64, device=t.device)
+    for i in range(0, flat.numel(), chunk):
+        bits = flat[i:i + chunk].long()
+        idx = torch.arange(i, i + bits.numel(), device=t.device, dtype=torch.int64)
+        total += ((bits + 40503) * (idx % 65521 + 1)).sum()
+    return int(total.item())
 
 
 def time_workload(name, steps, warmup, ratio=None):
