@@ -376,6 +376,29 @@ relaxkv_status relaxkv_query_attn(const relaxkv_problem* p, int32_t layer, const
                                   void* out, float* lse_out, void* ws, size_t ws_bytes,
                                   void* stream);
 
+/* Scratch that relaxkv_query_attn_noalloc holds on each GPU (a problem whose
+ * relaxkv_query_attn_workspace_bytes exceeds it is refused). */
+#define RELAXKV_QUERY_ATTN_NOALLOC_MAX_BYTES ((size_t)32 << 20)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph or
+ * stream capture, serving loops and harnesses that forbid hipMalloc):
+ * relaxkv_query_attn without a workspace argument.  Same arguments, kernels and
+ * results as relaxkv_query_attn; its scratch is a device array of
+ * RELAXKV_QUERY_ATTN_NOALLOC_MAX_BYTES inside the library, which each GPU it runs
+ * on holds until the process ends.  It calls no allocating routine.
+ * RELAXKV_ENOSPACE when relaxkv_query_attn_workspace_bytes(p) exceeds
+ * RELAXKV_QUERY_ATTN_NOALLOC_MAX_BYTES (e.g. bf16, H_kv 8, 64 query tokens x 5
+ * heads: 21 MB at any T_c up to 131072).  Every call on one GPU shares that GPU's
+ * scratch: calls that overlap on one device (other streams or threads) race and
+ * must be ordered by the caller.  Nothing in the scratch needs clearing: each
+ * call writes every element it reads.
+ */
+relaxkv_status relaxkv_query_attn_noalloc(const relaxkv_problem* p, int32_t layer,
+                                          const void* k_cache, const void* v_cache,
+                                          const void* k_q, const void* v_q, void* out,
+                                          float* lse_out, void* stream);
+
 /*
  * Synchronising.  Copies s->counts ([L+2] int32) to host_counts and, when
  * host_edges is not NULL, s->edges ([2L] int64) to host_edges, after all work

@@ -28,7 +28,9 @@ EXPORTS = ("relaxkv_status_string", "relaxkv_anchor_count", "relaxkv_validate",
            "relaxkv_score", "relaxkv_select", "relaxkv_build_sets", "relaxkv_build_sets_context",
            "relaxkv_select_global",
            "relaxkv_build_sets_global", "relaxkv_sparse_attn", "relaxkv_update_cache",
-           "relaxkv_query_attn_workspace_bytes", "relaxkv_query_attn", "relaxkv_counts_to_host")
+           "relaxkv_query_attn_workspace_bytes", "relaxkv_query_attn",
+           "relaxkv_query_attn_noalloc", "relaxkv_counts_to_host")
+QUERY_ATTN_NOALLOC_MAX_BYTES = 32 << 20
 
 
 class RelaxKVError(RuntimeError):
@@ -110,6 +112,9 @@ def load(path=None):
     lib.relaxkv_query_attn.restype = c_int32
     lib.relaxkv_query_attn.argtypes = [POINTER(Problem), c_int32, c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+    lib.relaxkv_query_attn_noalloc.restype = c_int32
+    lib.relaxkv_query_attn_noalloc.argtypes = [POINTER(Problem), c_int32, c_void_p, c_void_p,
+                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
     lib.relaxkv_counts_to_host.restype = c_int32
     lib.relaxkv_counts_to_host.argtypes = [POINTER(Sets), POINTER(c_int32), POINTER(c_int64),
                                            c_void_p]
@@ -348,6 +353,24 @@ class Request:
                                          _ptr(v_cache), _ptr(k_q), _ptr(v_q), _ptr(out),
                                          _ptr(lse_out), _ptr(ws), 0 if ws is None else _nbytes(ws),
                                          _stream(stream)), "relaxkv_query_attn")
+
+
+    def query_attn_noalloc(self, layer, k_cache, v_cache, k_q, v_q, out, lse_out=None,
+                           stream=None):
+        """query_attn through the allocation-free entry point (the library's own
+        per-GPU scratch; calls that overlap on one GPU race)."""
+        cache = (self.L, self.H_kv, self.T_c, self.d)
+        _need(k_cache, "k_cache", self.dtype, cache, self.device)
+        _need(v_cache, "v_cache", self.dtype, cache, self.device)
+        _need(k_q, "k_q", self.dtype, (self.n_query, self.H_kv, self.d), self.device)
+        _need(v_q, "v_q", self.dtype, (self.n_query, self.H_kv, self.d), self.device)
+        _need(out, "out", self.dtype, (self.n_query, self.H, self.d), self.device)
+        if lse_out is not None:
+            _need(lse_out, "lse_out", torch.float32, (self.n_query, self.H), self.device)
+        _check(load().relaxkv_query_attn_noalloc(ctypes.byref(self.p), int(layer), _ptr(k_cache),
+                                                 _ptr(v_cache), _ptr(k_q), _ptr(v_q), _ptr(out),
+                                                 _ptr(lse_out), _stream(stream)),
+               "relaxkv_query_attn_noalloc")
 
 
 class SetsBuffer:

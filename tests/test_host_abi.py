@@ -312,3 +312,30 @@ def test_binding_checks_tensors_before_any_call(rk):
     kc = torch.zeros(2, 2, 32, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="device tensor"):
         rk.Request(q, kc, kc.clone(), 0.15)
+
+
+def test_query_attn_noalloc_rejects_before_any_device_call(rk):
+    """The allocation-free query-side completion validates like relaxkv_query_attn
+    and refuses a problem whose scratch exceeds what it holds, before it touches
+    a device (every call here is refused)."""
+    lib = rk.load()
+    fake = ctypes.c_void_p(0x7e0000000000)
+    cap = rk.QUERY_ATTN_NOALLOC_MAX_BYTES
+    big = _problem(rk, T_c=1 << 19, n_query=64, H=40, H_kv=8)
+    assert lib.relaxkv_query_attn_workspace_bytes(ctypes.byref(big)) > cap
+    qn = lib.relaxkv_query_attn_noalloc
+    assert qn(ctypes.byref(big), 0, fake, fake, fake, fake, fake, None, None) == rk.ENOSPACE
+    p = _problem(rk)
+    for layer in (-1, 4):
+        assert qn(ctypes.byref(p), layer, fake, fake, fake, fake, fake, None, None) == rk.EINVAL
+    for i in range(5):
+        ptrs = [fake] * 5
+        ptrs[i] = None
+        assert qn(ctypes.byref(p), 0, *ptrs, None, None) == rk.EINVAL
+    assert qn(ctypes.byref(_problem(rk, d=96)), 0, fake, fake, fake, fake, fake, None,
+              None) == rk.EUNSUPPORTED
+    assert qn(None, 0, fake, fake, fake, fake, fake, None, None) == rk.EINVAL
+    # the bound the header states: 40q/8kv heads, 64 query tokens, T_c up to 131072
+    for T in (4096, 32768, 131072):
+        fits = _problem(rk, T_c=T, n_query=64, H=40, H_kv=8)
+        assert 0 < lib.relaxkv_query_attn_workspace_bytes(ctypes.byref(fits)) <= cap
