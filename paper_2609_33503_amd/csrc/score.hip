@@ -11,9 +11,9 @@
 //   1. score_stats_kreg -- S^T = K Q^T (one query row per lane): each row's
 //      (reference, sum of exp2) over the split.           [skipped with q_lse]
 //   2. score_merge  -- per row, merge the splits into a log2-sum-exp.
-//   3. score_colsum_kreg -- S = Q K^T - lse (one key per lane; the row's -lse
-//      rides as an extra k-step), summing exp2 over the rows: the pooled mass
-//      of each key for this KV head.
+//   3. score_colsum_kreg -- S = Q K^T - lse (one key per lane; each
+//      accumulator starts at its row's -lse), summing exp2 over the rows: the
+//      pooled mass of each key for this KV head.
 //   4. score_pool / score_minmax -- the fixed-order sum over KV heads and the
 //      1/(H Qn) factor with per-block extrema, then the MinMax normalisation.
 // float32 path: plain VALU kernels with the same four steps (used for fp32
@@ -33,10 +33,10 @@ namespace {
 #define RELAXKV_SCORE_SPLIT 4096              // keys per workgroup
 #endif
 #ifndef RELAXKV_SCORE_KREG_NW
-#define RELAXKV_SCORE_KREG_NW 8               // waves per workgroup
+#define RELAXKV_SCORE_KREG_NW 16              // waves per workgroup (four per SIMD)
 #endif
 #ifndef RELAXKV_SCORE_KREG_NKB
-#define RELAXKV_SCORE_KREG_NKB 2              // 32-key blocks per wave and round
+#define RELAXKV_SCORE_KREG_NKB 1              // 32-key blocks per wave and round
 #endif
 constexpr int kKeysPerSplit = RELAXKV_SCORE_SPLIT;
 constexpr int kKregRowBlocks = 10;            // 32-row blocks staged per row chunk
@@ -66,44 +66,39 @@ __device__ __forceinline__ float pair_other(float x) {
 // Stage rows rc0 .. rc0 + 32 nrb - 1 of the row set (l, g) into Qs, fragment-major:
 // fragment (rb, j) holds the MFMA operand of 32-row block rb and k-step j (lane
 // l: row 32 rb + l % 32, 16-byte chunk 2j + l / 32; padding rows are zero).
-// With LSE, k-step KS of each block carries -lse2 / sl2 of the lane's row as
-// three bf16 terms in its first three k-slots (lanes 0-31; zero elsewhere).
-template <int D, int NW, bool LSE>
+template <int D, int NW>
 __device__ __forceinline__ void stage_rows(bf16x8* Qs, const uint16_t* __restrict__ q, int l,
-                                           int g, int Qn, int H, int Hkv, int G, int n_rows,
-                                           int rows_pad, int rc0, int nrb, float sl2,
-                                           const float* __restrict__ lse2,
-                                           const float* __restrict__ q_lse) {
+                                           int g, int Qn, int H, int G, int n_rows, int rc0,
+                                           int nrb) {
     constexpr int KS = D / 16;
-    constexpr int KF = LSE ? KS + 1 : KS;
-    for (int f = threadIdx.x; f < nrb * KF * 64; f += NW * 64) {
-        const int ln = f & 63, fj = f >> 6, rb = fj / KF, j = fj - rb * KF;
+    for (int f = threadIdx.x; f < nrb * KS * 64; f += NW * 64) {
+        const int ln = f & 63, fj = f >> 6, rb = fj / KS, j = fj - rb * KS;
         const int row = rc0 + rb * 32 + (ln & 31), h2 = ln >> 5;
         bf16x8 v = {};
-        if (j < KS) {
-            if (row < n_rows) {
-                const int t = row / G, hh = row - (row / G) * G;
-                v = *(const bf16x8*)(q + (((size_t)l * Qn + t) * H + g * G + hh) * D + 16 * j +
-                                     8 * h2);
-            }
-        } else if (h2 == 0) {
-            const float x = row >= n_rows ? INFINITY
-                            : q_lse ? q_lse[((size_t)l * Qn + row / G) * H + g * G + row % G] * kLog2e
-                                    : lse2[((size_t)l * Hkv + g) * rows_pad + row];
-            const float y = -x / sl2;
-            if (fabsf(y) < INFINITY) {
-                const uint16_t b1 = f32_to_bf16_bits(y);
-                const float r1 = y - bf16_bits_to_f32(b1);
-                const uint16_t b2 = f32_to_bf16_bits(r1);
-                const uint16_t b3 = f32_to_bf16_bits(r1 - bf16_bits_to_f32(b2));
-                v[0] = __builtin_bit_cast(__bf16, b1);
-                v[1] = __builtin_bit_cast(__bf16, b2);
-                v[2] = __builtin_bit_cast(__bf16, b3);
-            } else {
-                v[0] = __builtin_bit_cast(__bf16, f32_to_bf16_bits(y));   // -inf: row adds 0
-            }
+        if (row < n_rows) {
+            const int t = row / G, hh = row - t * G;
+            v = *(const bf16x8*)(q + (((size_t)l * Qn + t) * H + g * G + hh) * D + 16 * j + 8 * h2);
         }
         Qs[f] = v;
+    }
+}
+
+// The accumulator start values of the column-sum pass: Ls[rb][hf][i] = -lse2 / sl2
+// of row rc0 + 32 rb + 8 (i / 4) + 4 hf + i % 4, the row that element i of an
+// S = Q K^T accumulator of row block rb holds in lane half hf; -inf for padding
+// rows (their probabilities are then exp2(-inf) = 0).
+__device__ __forceinline__ void stage_lse(float (*Ls)[2][16], int nt, int l, int g, int Qn,
+                                          int H, int Hkv, int G, int n_rows, int rows_pad,
+                                          int rc0, int nrb, float sl2,
+                                          const float* __restrict__ lse2,
+                                          const float* __restrict__ q_lse) {
+    for (int f = threadIdx.x; f < nrb * 32; f += nt) {
+        const int rb = f >> 5, hh = (f >> 4) & 1, i = f & 15;
+        const int row = rc0 + 32 * rb + 8 * (i >> 2) + 4 * hh + (i & 3);
+        const float x = row >= n_rows ? INFINITY
+                        : q_lse ? q_lse[((size_t)l * Qn + row / G) * H + g * G + row % G] * kLog2e
+                                : lse2[((size_t)l * Hkv + g) * rows_pad + row];
+        Ls[rb][hh][i] = -x / sl2;
     }
 }
 
@@ -127,9 +122,9 @@ __device__ __forceinline__ void load_keys(bf16x8 (&dst)[NKB][D / 16], const uint
 // group are staged once into LDS, fragment-major: fragment (rb, j) is the MFMA A
 // operand of 32-row block rb and k-step j, lane l's 16 bytes at 16 l, so every
 // read is one conflict-free ds_read_b128 at a fixed offset from the lane's base.
-// The last k-step carries the row's -lse2 / sl2 as three bf16 terms (their sum
-// is the fp32 value exactly) against a constant B fragment of ones, so the
-// accumulator ends at s - lse2 / sl2 and exp2(sl2 * acc) is the probability.
+// Each accumulator starts at its rows' -lse2 / sl2 (the C operand of the first
+// MFMA, read from a small LDS table; the lanes of a half read the same 64
+// bytes), so it ends at s - lse2 / sl2 and exp2(sl2 * acc) is the probability.
 // Each wave owns NKB blocks of 32 keys per round, loads them from HBM straight
 // into registers (the B operand of S = Q K^T: lane l holds key l % 32, the
 // 16-byte chunk 2j + l / 32 of k-step j) and runs every row block against them,
@@ -145,11 +140,11 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
     int Hkv, int G, int n_rows, int rows_pad, int keys_per_split, float sl2,
     const float* __restrict__ lse2, const float* __restrict__ q_lse, float* __restrict__ part) {
     constexpr int KS = D / 16;                      // k-steps of the dot product
-    constexpr int KF = KS + 1;                      // plus the -lse2 / sl2 step
     constexpr int NRB = kKregRowBlocks;             // row blocks per chunk
     constexpr int KPW = NKB * 32;                   // keys of a wave per round
     constexpr int KPR = NW * KPW;                   // keys of the workgroup per round
-    __shared__ bf16x8 Qs[NRB * KF * 64];
+    __shared__ bf16x8 Qs[NRB * KS * 64];
+    __shared__ __attribute__((aligned(64))) float Ls[NRB][2][16];
 
     const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, hf = lane >> 5;
@@ -158,8 +153,6 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
     float* part_g = part + ((size_t)l * Hkv + g) * T;
     const int key0 = split * keys_per_split;
     const int key1 = min(T, key0 + keys_per_split);
-    bf16x8 ones = {};
-    if (hf == 0) ones[0] = ones[1] = ones[2] = (__bf16)1.0f;
 
     bf16x8 kf[NKB][KS];
     auto load_k = [&](bf16x8 (&dst)[NKB][KS], int kr) { load_keys<D, NKB>(dst, Kg, T, kr, r32, hf); };
@@ -167,7 +160,8 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
     for (int rc0 = 0; rc0 < rows_pad; rc0 += NRB * 32) {
         const int nrb = min(NRB, (rows_pad - rc0) / 32);
         __syncthreads();                             // the previous chunk's reads are done
-        stage_rows<D, NW, true>(Qs, q, l, g, Qn, H, Hkv, G, n_rows, rows_pad, rc0, nrb, sl2, lse2, q_lse);
+        stage_rows<D, NW>(Qs, q, l, g, Qn, H, G, n_rows, rc0, nrb);
+        stage_lse(Ls, NW * 64, l, g, Qn, H, Hkv, G, n_rows, rows_pad, rc0, nrb, sl2, lse2, q_lse);
         __syncthreads();
 
         // One round: the wave's NKB key blocks (in kfr) against every row block;
@@ -180,14 +174,15 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
             for (int rb = 0; rb < NRB; ++rb) {
                 if (rb >= nrb) break;
                 f32x16 acc[NKB];
-                const bf16x8* qb = Qs + rb * KF * 64 + lane;
+                const f32x16 init = *(const f32x16*)&Ls[rb][hf][0];
+                const bf16x8* qb = Qs + rb * KS * 64 + lane;
 #pragma unroll
-                for (int j = 0; j < KF; ++j) {
+                for (int j = 0; j < KS; ++j) {
                     const bf16x8 qj = qb[j * 64];
 #pragma unroll
                     for (int kb = 0; kb < NKB; ++kb)
                         acc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            qj, j < KS ? kfr[kb][j] : ones, j == 0 ? f32x16{} : acc[kb], 0, 0, 0);
+                            qj, kfr[kb][j], j == 0 ? init : acc[kb], 0, 0, 0);
                 }
                 hook(rb);
 #pragma unroll
@@ -245,8 +240,7 @@ __global__ __launch_bounds__(NW * 64) void score_stats_kreg(
     for (int rc0 = 0; rc0 < rows_pad; rc0 += NRB * 32) {
         const int nrb = min(NRB, (rows_pad - rc0) / 32);
         __syncthreads();                             // the previous chunk's reads are done
-        stage_rows<D, NW, false>(Qs, q, l, g, Qn, H, Hkv, G, n_rows, rows_pad, rc0, nrb, sl2,
-                                 nullptr, nullptr);
+        stage_rows<D, NW>(Qs, q, l, g, Qn, H, G, n_rows, rc0, nrb);
         __syncthreads();
 
         float m_ref[NRB], z_run[NRB];
