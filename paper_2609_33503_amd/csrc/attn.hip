@@ -145,6 +145,10 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
                                ((size_t)(valid ? t_row : t0) * a.H + (valid ? head : 0)) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
+        // Consumed here, so the compiler's waits for these loads stay before the
+        // loop: inside it they would also wait for the K/V fills just issued.
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(qf[ks]));
     }
     f32x16 o[DB];
 #pragma unroll
@@ -152,10 +156,11 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     float m_run = lim < 0 ? 0.f : -INFINITY;       // empty context: every p is exp2(-inf) = 0
     float l_run = 0.f;
 
-    const uint16_t* kng = (const uint16_t*)a.k_new + (size_t)g * D;     // fresh rows: stride Hkv*D
-    const uint16_t* kcg = (const uint16_t*)a.kc + (size_t)g * a.T * D;  // cached rows: stride D
-    const long dv_fresh = (const uint16_t*)a.v_new - (const uint16_t*)a.k_new;
-    const long dv_cached = (const uint16_t*)a.vc - (const uint16_t*)a.kc;
+    // Row bases of the fresh rows (stride Hkv*D) and of the cached layer (stride D).
+    const uint16_t* kng = (const uint16_t*)a.k_new + (size_t)g * D;
+    const uint16_t* vng = (const uint16_t*)a.v_new + (size_t)g * D;
+    const uint16_t* kcg = (const uint16_t*)a.kc + (size_t)g * a.T * D;
+    const uint16_t* vcg = (const uint16_t*)a.vc + (size_t)g * a.T * D;
     const int32_t* srcmap = FULL ? a.rank_l : a.src_l;
     const int S = cmax / TK + 1;                     // 64-key steps
 
@@ -168,22 +173,38 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
             fill_lds4(src, lds_addr(&Ix[m & 3][ww][0]));
         }
     };
+    // The lane's tile row and swizzled chunk offset (elements) in each of its
+    // fills: loop invariant.
+    int f_row[PPW];
+    uint32_t f_choff[PPW];
+#pragma unroll
+    for (int i = 0; i < PPW; ++i) {
+        f_row[i] = (w + i * NW) * RPI + lane / CH;
+        f_choff[i] = (uint32_t)(((lane % CH) ^ tile_swz<D>(f_row[i])) << 3);
+    }
     auto issue_rows = [&](int m) {
-        int lr = lane / CH, pc = lane % CH, ww = w;
-        asm volatile("" : "+v"(lr), "+v"(pc), "+s"(ww));
         const int st = m & 3;
 #pragma unroll
         for (int i = 0; i < PPW; ++i) {
-            const int j = ww + i * NW;
+            const int j = w + i * NW;
             if (NL % NW == 0 || j < NL) {
-                const int row = j * RPI + lr;
+                int row = f_row[i];
+                uint32_t choff = f_choff[i];
+                asm volatile("" : "+v"(row), "+v"(choff));
                 const int c = m * TK + row;
-                const int pos = FULL ? min(c, cmax) : Ix[st][0][row];
-                const int r = Ix[st][FULL ? 0 : 1][row];
+                int pos = FULL ? min(c, cmax) : Ix[st][0][row];
+                int r = Ix[st][FULL ? 0 : 1][row];
+                asm volatile("" : "+v"(pos), "+v"(r));      // both read, then selected
+                // (the empty asm statements keep the compiler from turning the
+                // fresh/cached choice into a divergent branch)
                 const bool fresh = r >= 0;
-                const uint16_t* kp = (fresh ? kng + (size_t)r * (Hkv * D) : kcg + (size_t)pos * D) +
-                                     ((pc ^ tile_swz<D>(row)) << 3);
-                const uint16_t* vp = kp + (fresh ? dv_fresh : dv_cached);
+                // element offset of the row's chunk (< 2^31: T_c * D and |R_l| * Hkv * D)
+                const uint32_t off = (fresh ? (uint32_t)r * (uint32_t)(Hkv * D)
+                                            : (uint32_t)pos * (uint32_t)D) + choff;
+                const uint64_t kb = fresh ? (uint64_t)kng : (uint64_t)kcg;
+                const uint64_t vb = fresh ? (uint64_t)vng : (uint64_t)vcg;
+                const uint16_t* kp = (const uint16_t*)kb + off;
+                const uint16_t* vp = (const uint16_t*)vb + off;
                 fill_lds16(kp, lds_addr(Kt[st] + j * RPI * D));
                 fill_lds16(vp, lds_addr(Vt[st] + j * RPI * D));
             }
@@ -220,9 +241,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
         // S^T = K Q^T: s[kb][v] = S[row][key 64 j + 32 kb + 8(v/4) + 4 hf + v%4]
         f32x16 s[2];
         {
-            int kbo = k_base;
+            int kbo = k_base + (j & 3) * (TK * D * 2);    // the stage offset leaves the swizzled bits alone
             asm volatile("" : "+v"(kbo));
-            const char* kst = (const char*)Kt[j & 3];
+            const char* kst = (const char*)Kt[0];
             s[0] = s[1] = f32x16{};
             // K fragments x = 2 ks + kb, read KA ahead of their MFMA.
             constexpr int KA = RELAXKV_ATTN_KAHEAD < 2 * KS ? RELAXKV_ATTN_KAHEAD : 2 * KS;
@@ -325,9 +346,11 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
 #endif
         // O^T += V^T P^T
         {
-            int vb0 = v_base0, vb1 = v_base1;
+            // LDS byte addresses of the lane's two V rows in this step's tile: the
+            // tile base and stage only set bits above the swizzled chunk bits.
+            const uint32_t vstage = lds_addr(Vt[0]) + (uint32_t)(j & 3) * (TK * D * 2);
+            uint32_t vb0 = v_base0 + vstage, vb1 = v_base1 + vstage;
             asm volatile("" : "+v"(vb0), "+v"(vb1));
-            const char* vst = (const char*)Vt[j & 3];
 #if RELAXKV_ATTN_SETPRIO
             __builtin_amdgcn_s_setprio(2);
 #endif
@@ -337,11 +360,11 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
                 for (int db = 0; db < DB; ++db)
 #pragma unroll
                     for (int k2 = 0; k2 < 2; ++k2) {
-                        const char* rowp = vst + (kb * 32 + k2 * 16) * ROWB;
-                        const v4i16 a0 =
-                            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(rowp + (vb0 ^ (db << 6))));
-                        const v4i16 a1 =
-                            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(rowp + (vb1 ^ (db << 6))));
+                        const uint32_t rowo = (kb * 32 + k2 * 16) * ROWB;
+                        const v4i16 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_v4i16*)(uintptr_t)((vb0 ^ (db << 6)) + rowo));
+                        const v4i16 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_v4i16*)(uintptr_t)((vb1 ^ (db << 6)) + rowo));
                         const bf16x8 vv =
                             __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
                         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pb[kb][k2], o[db], 0, 0, 0);
@@ -372,6 +395,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     if (a.lse && hf == 0)
         a.lse[(size_t)t_row * a.H + head] = empty ? -INFINITY : (m_run + __log2f(l_tot)) * kLn2;
 }
+
 
 // ----------------------------------------------------------------- fp32 VALU
 
