@@ -103,6 +103,9 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
         const uint16_t* qrow = a.q + ((size_t)t_row * a.H + g * a.G + hh) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
+        // Consumed here, so the compiler's waits for these loads stay before the loop.
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(qf[ks]));
     }
     f32x16 o[DB];
 #pragma unroll
@@ -138,6 +141,35 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
             }
         }
     };
+    // Full cache tiles (all but the split's tail tile and the query tiles): the
+    // lane's source of load i is a loop-invariant base plus the tile offset.
+    const uint16_t* cbase[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        const int j = w + i * NW;
+        const bool isv = j >= NL;
+        const int jj = isv ? j - NL : j;
+        const int row = jj * RPI + lrow;
+        cbase[i] = (isv ? a.vc : a.kc) + ((size_t)g * a.T + key0 + row) * D +
+                   ((pchunk ^ tile_swz<D>(row)) << 3);
+    }
+    auto issue_full = [&](int tt) {
+        const int st = tt % kQaStages;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int j = w + i * NW;
+            if (i < LPW || j < NL2) {
+                const bool isv = j >= NL;
+                const int jj = isv ? j - NL : j;
+                uint16_t* dst = (isv ? Vt[st] : Kt[st]) + jj * RPI * D;
+                load_lds16(cbase[i] + (size_t)tt * TK * D, dst);
+            }
+        }
+    };
+    auto issue = [&](int tt) {
+        if ((tt + 1) * TK <= nkc) issue_full(tt);
+        else issue_tile(tt);
+    };
     // rem = tiles issued after the one needed now: each wave issued at least
     // LPW loads per tile after it (in-order completion).
     auto wait_tile = [&](int rem) {
@@ -155,15 +187,19 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
 
 #pragma unroll
     for (int tt = 0; tt < kQaStages - 1; ++tt)
-        if (tt < ntile) issue_tile(tt);
+        if (tt < ntile) issue(tt);
     for (int tt = 0; tt < ntile; ++tt) {
         wait_tile(min(kQaStages - 2, ntile - 1 - tt));
-        if (tt + kQaStages - 1 < ntile) issue_tile(tt + kQaStages - 1);
-        const char* kst = (const char*)Kt[tt % kQaStages];
-        const char* vst = (const char*)Vt[tt % kQaStages];
-        // Fragment offsets made opaque per tile (recomputed with a few XORs
-        // rather than held in registers across the loop).
-        int kbo = k_base, vb0 = v_base0, vb1 = v_base1;
+        if (tt + kQaStages - 1 < ntile) issue(tt + kQaStages - 1);
+        // Fragment byte addresses of this tile's ring stage: the stage (and the V
+        // tile base) only set bits above the swizzled chunk bits, so one add per
+        // tile and one xor per fragment address; made opaque per tile so they
+        // are recomputed rather than held in registers across the loop.
+        const char* kst = (const char*)Kt[0];
+        const uint32_t stage = (uint32_t)(tt % kQaStages) * (TK * D * 2);
+        const uint32_t vstage = lds_addr(Vt[0]) + stage;
+        int kbo = k_base + (int)stage;
+        uint32_t vb0 = v_base0 + vstage, vb1 = v_base1 + vstage;
         asm volatile("" : "+v"(kbo), "+v"(vb0), "+v"(vb1));
         const bool qt = tt >= ntc;
         const int c0 = qt ? (tt - ntc) * TK : tt * TK;
@@ -237,11 +273,11 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
             for (int db = 0; db < DB; ++db)
 #pragma unroll
                 for (int k2 = 0; k2 < 2; ++k2) {
-                    const char* rowp = vst + (kb * 32 + k2 * 16) * ROWB;
+                    const uint32_t rowo = (kb * 32 + k2 * 16) * ROWB;
                     const v4i16 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        (lds_v4i16*)(rowp + (vb0 ^ (db << 6))));
+                        (lds_v4i16*)(uintptr_t)((vb0 ^ (db << 6)) + rowo));
                     const v4i16 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        (lds_v4i16*)(rowp + (vb1 ^ (db << 6))));
+                        (lds_v4i16*)(uintptr_t)((vb1 ^ (db << 6)) + rowo));
                     const bf16x8 vv = __builtin_bit_cast(
                         bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
                     o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pb[kb][k2], o[db], 0, 0, 0);
