@@ -25,6 +25,10 @@ Other objects:
   ratios 0.05 / 0.15 / 0.30) with their set statistics;
 - "anchor_jaccard_gpu_vs_oracle_scores": anchors from the library's scores
   against anchors from the oracle's float64 scores on sampled layers;
+- "clock": each XCD's graphics clock and the socket power while the step runs
+  (the attention holds the chip near 1.9 GHz, below its 2.4 GHz maximum); the
+  roofline adds the fraction of the peak scaled to that clock, and "scoring"
+  its MFMA and exp2 issue bounds next to the HBM bound;
 - "cpu_baseline": the float64 oracle, stage by stage, on this host's cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
@@ -599,6 +603,93 @@ def cpu_baseline(b: Bench, budget_s=15.0):
             "cpu_model": _cpu_model()}
 
 
+def _smi_handle():
+    """amdsmi handle of cuda:0 (matched by PCI address), or None."""
+    import amdsmi
+    amdsmi.amdsmi_init()
+    handles = amdsmi.amdsmi_get_processor_handles()
+    props = torch.cuda.get_device_properties(0)
+    want = f"{props.pci_domain_id:04x}:{props.pci_bus_id:02x}:{props.pci_device_id:02x}"
+    for h in handles:
+        if str(amdsmi.amdsmi_get_gpu_device_bdf(h)).lower().startswith(want):
+            return h
+    return handles[0] if len(handles) == 1 else None
+
+
+def held_clock(b: Bench, seconds=2.5):
+    """Graphics clock of each XCD and socket power while the benchmark step runs.
+
+    The device's metrics table (amdsmi) is sampled every 20 ms from a host thread
+    while whole steps run back to back for about `seconds`; clocks are the
+    median of the samples taken after the first 0.6 s (the table refreshes
+    about once a second), power is the energy counter's difference over the
+    run's wall time.  The attention holds the chip below its 2.4 GHz maximum,
+    so its fraction of the spec peak understates its use of the MFMA pipe."""
+    import threading
+    try:
+        import amdsmi
+        h = _smi_handle()
+        if h is None:
+            return {"available": False, "reason": "no amdsmi handle for cuda:0"}
+        amdsmi.amdsmi_get_gpu_metrics_info(h)
+    except Exception as e:                                   # noqa: BLE001
+        return {"available": False, "reason": f"amdsmi: {e}"}
+    samples, stop = [], threading.Event()
+
+    def poll():
+        while not stop.is_set():
+            try:
+                m = amdsmi.amdsmi_get_gpu_metrics_info(h)
+            except Exception:                                # noqa: BLE001
+                break
+            clks = m.get("current_gfxclks")
+            if isinstance(clks, list):
+                clks = [c for c in clks if isinstance(c, (int, float)) and 0 < c < 10000]
+            samples.append((time.perf_counter(), clks or [], m.get("temperature_hotspot")))
+            stop.wait(0.02)
+
+    b.step()
+    torch.cuda.synchronize()
+    try:
+        e0 = amdsmi.amdsmi_get_energy_count(h)
+    except Exception:                                        # noqa: BLE001
+        e0 = None
+    th = threading.Thread(target=poll, daemon=True)
+    t0 = time.perf_counter()
+    th.start()
+    steps = 0
+    while time.perf_counter() - t0 < seconds:
+        b.step()
+        torch.cuda.synchronize()
+        steps += 1
+    t1 = time.perf_counter()
+    try:
+        e1 = amdsmi.amdsmi_get_energy_count(h)
+    except Exception:                                        # noqa: BLE001
+        e1 = None
+    stop.set()
+    th.join()
+    late = [c for t, c, _ in samples if t - t0 > 0.6 and c]
+    if not late:
+        return {"available": False, "reason": "no clock samples"}
+    by_xcd = [float(np.median([c[i] for c in late if len(c) > i])) for i in range(len(late[0]))]
+    res = {"available": True, "gfxclk_mhz_by_xcd": by_xcd,
+           "gfxclk_mhz_mean": float(np.mean(by_xcd)), "gfxclk_mhz_max_spec": 2400,
+           "steps": steps, "seconds": t1 - t0, "samples": len(late),
+           "hotspot_c_max": max((x for _, _, x in samples if isinstance(x, (int, float))),
+                                default=None),
+           "source": "amdsmi GPU metrics (per-XCD current graphics clock, energy counter) "
+                     "sampled while whole benchmark steps run back to back"}
+    try:
+        joules = (e1["energy_accumulator"] - e0["energy_accumulator"]) * e0["counter_resolution"] * 1e-6
+        if joules > 0:
+            res["socket_power_w"] = joules / (t1 - t0)
+            res["energy_j_per_step"] = joules / steps
+    except Exception:                                        # noqa: BLE001
+        pass
+    return res
+
+
 def scoring_report(w, ms_two_pass, ms_one_pass):
     """Algorithmic HBM bytes of relaxkv_score (K read once per layer, Q, the
     supplied LSE, the fp32 scores) over the measured time, both modes."""
@@ -606,7 +697,19 @@ def scoring_report(w, ms_two_pass, ms_one_pass):
     lse_bytes = w.L * w.Qn * w.H * 4
     gbs2 = nbytes / (ms_two_pass * 1e-3) / 1e9
     gbs1 = (nbytes + lse_bytes) / (ms_one_pass * 1e-3) / 1e9
-    return {"self_contained_ms": ms_two_pass, "self_contained_gbs": gbs2,
+    # Issue bounds of one layer at the spec peaks: the QK^T contraction on the
+    # bf16 MFMA pipe and the exp2 of every (query row, key) on the transcendental
+    # unit (one wave64 v_exp_f32 per 8 cycles per SIMD, 1024 SIMDs, 2.4 GHz).
+    # The self-contained mode makes both passes over K, so twice each.
+    flops1 = 2.0 * w.Qn * w.H * w.T_c * w.d
+    exps1 = float(w.Qn * w.H * w.T_c)
+    bounds = {"hbm_us": 1e6 * (nbytes / w.L) / (PEAK_HBM_GBS * 1e9),
+              "mfma_us_one_pass": 1e6 * flops1 / (PEAK_BF16_TFLOPS * 1e12),
+              "exp2_us_one_pass": 1e6 * exps1 / (1024 * 8 * 2.4e9),
+              "mfma_us_self_contained": 2e6 * flops1 / (PEAK_BF16_TFLOPS * 1e12),
+              "exp2_us_self_contained": 2e6 * exps1 / (1024 * 8 * 2.4e9)}
+    return {"bounds_us_per_layer_at_spec": bounds,
+            "self_contained_ms": ms_two_pass, "self_contained_gbs": gbs2,
             "self_contained_hbm_frac": gbs2 / PEAK_HBM_GBS,
             "supplied_lse_ms": ms_one_pass, "supplied_lse_gbs": gbs1,
             "supplied_lse_hbm_frac": gbs1 / PEAK_HBM_GBS,
@@ -707,6 +810,17 @@ def main():
                      "frac_of_measured_gemm": attn_tflops / peaks["gemm_bf16_tflops"]},
         "measured_peaks": peaks,
     }
+    clk = held_clock(b)
+    res["clock"] = clk
+    if clk.get("available"):
+        f = clk["gfxclk_mhz_mean"] / 2400.0
+        res["roofline"]["peak_at_held_clock"] = peak * f
+        res["roofline"]["frac_at_held_clock"] = attn_tflops / (peak * f)
+        bnd = scoring["bounds_us_per_layer_at_spec"]
+        scoring["bounds_us_per_layer_at_held_clock"] = {
+            k: (v if k == "hbm_us" else v / f) for k, v in bnd.items()}
+        if "energy_j_per_step" in clk:
+            clk["tflop_per_joule"] = flops / 1e12 / clk["energy_j_per_step"]
     res["cache_update"] = time_cache_update(b)
     if not args.no_matched_targets:
         res["matched_targets"] = time_matched_targets(b)

@@ -143,6 +143,11 @@ typedef struct relaxkv_problem {
  *                          of a row, ascending): row 0 for every layer (Global Sparse) or
  *                          row l for layer l (Layerwise Sparse); unused for the union.
  *   g        [T_c]         float32 layer-mean scores of the last Global Sparse build.
+ *   tiles    [2][L][H_kv+1] uint32 work counters of the bf16 attention, one slot per
+ *                          context mode (0: the layer's context list, 1: Full-Prefix
+ *                          Control) and layer: a next-tile counter per KV head and a
+ *                          count of the launch's workgroups.  Zeroed by every set build;
+ *                          each relaxkv_sparse_attn launch returns its slot to zero.
  *   k        the anchor budget k = max(1, round(r T_c)), computed on the host.
  *   global_targets  host flag: 0 after relaxkv_sets_bind and relaxkv_build_sets
  *                   (targets R_l of RelaxKV, |R_l| <= min(T_c, (L-l) k)), 1 after
@@ -169,6 +174,7 @@ typedef struct relaxkv_sets {
     int64_t* edges;
     int32_t* ctx;
     float* g;
+    uint32_t* tiles;
     int32_t global_targets;
     int32_t context_sets;
 } relaxkv_sets;
@@ -319,6 +325,10 @@ relaxkv_status relaxkv_build_sets_global(const relaxkv_problem* p, relaxkv_sets*
  * naive cache of the layer is read from p->k_cache / p->v_cache.  A target
  * whose context is empty (only with relaxkv_build_sets_global, union context)
  * gets O = 0 and lse = -inf.
+ * The bf16 kernel's workgroups take their tiles from the s->tiles slot of this
+ * layer and context mode (dynamic balancing across XCDs whose clocks differ):
+ * two launches with the same sets, layer and context mode must not overlap in
+ * time (stream-ordered calls are fine); launches for other layers or modes may.
  */
 relaxkv_status relaxkv_sparse_attn(const relaxkv_problem* p, const relaxkv_sets* s,
                                    int32_t layer, const void* q_new, const void* k_new,

@@ -23,8 +23,10 @@
 // - the mask is the staircase of the targets' limits: steps below the first
 //   target's limit run unmasked, the rest compare each key with its row's limit;
 // - tiles are taken heaviest-first (the last targets have the longest
-//   contexts) and consecutive workgroups cycle through the KV heads, so the
-//   workgroups that land on one XCD share a KV head and its L2 working set.
+//   contexts) from per-KV-head counters; a workgroup starts with the head tied
+//   to its XCD, so the workgroups of one XCD share a KV head and its L2
+//   working set, and takes the next head's tiles once its own are gone (the
+//   XCDs run at different clocks, and a fixed map would wait for the slowest).
 // fp32 kernel: one wave per (target, head), VALU dot products and an online
 // softmax across the wave; used for fp32 inputs, where bf16 MFMA would not meet
 // fp32 accuracy.
@@ -52,6 +54,7 @@ struct AttnArgs {
     const int32_t* R_u;
     const int32_t* counts;
     int32_t* err;            // the error word counts[L+1]
+    uint32_t* tiles;         // this layer's and mode's work counters: [Hkv] next tile, [Hkv] workgroups
     void* out;
     float* lse;
     int H, Hkv, G, T, layer, BT;
@@ -78,6 +81,8 @@ __device__ __forceinline__ size_t kv_row(const AttnArgs& a, int c, int g, bool& 
 // ----------------------------------------------------------------- bf16 MFMA
 
 constexpr float kRescaleSlack = 8.0f;      // log2 units the running max may lag the true max
+constexpr int kXcds = 8;                   // XCDs of an MI355X (workgroup i runs on XCD i mod 8)
+constexpr int kHwRegXccId = 20;            // hardware register holding the wave's XCD index
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -111,15 +116,45 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     __shared__ __attribute__((aligned(1024))) uint16_t Vt[NST][TK * D];
     __shared__ __attribute__((aligned(256))) int32_t Ix[NST][2][TK];   // [U or rank, src]
 
+    __shared__ int s_pick;
+
     const int Hkv = a.Hkv;
-    const int g = blockIdx.x % Hkv;
-    const int tile_rev = blockIdx.x / Hkv;
     const int nR_dev = a.counts[1 + a.layer];
     const int nR = min(nR_dev, a.cap);
     if (nR_dev > a.cap && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(a.err, RELAXKV_ERR_ROWS);
     const int ntiles = (nR + a.BT - 1) / a.BT;
-    if (tile_rev >= ntiles) return;
-    const int tile = ntiles - 1 - tile_rev;          // heaviest tiles first
+    // Tile choice.  Each KV head's tiles are handed out heaviest first from its
+    // counter; a workgroup starts with a head tied to its XCD (so the
+    // workgroups of one XCD share that head's K/V in their L2) and moves on to
+    // the next head once that one is exhausted.  The XCDs run at different
+    // clocks, so a fixed blockIdx -> tile map would make every launch wait for
+    // the slowest; the grid carries spare workgroups for the faster ones.  The
+    // last workgroup to take its pick returns the counters to zero for the
+    // next launch of this layer and mode.
+    if (threadIdx.x == 0) {
+        const int xcc = (int)__builtin_amdgcn_s_getreg(kHwRegXccId | ((4 - 1) << 11));
+        int h = (xcc + kXcds * (int)((blockIdx.x / kXcds) % ((Hkv + kXcds - 1) / kXcds))) % Hkv;
+        int pick = -1;
+        for (int tried = 0; tried < Hkv; ++tried) {
+            const int t = (int)atomicAdd(a.tiles + h, 1u);
+            if (t < ntiles) {
+                pick = t * Hkv + h;
+                break;
+            }
+            h = h + 1 == Hkv ? 0 : h + 1;
+        }
+        s_pick = pick;
+        __threadfence();
+        if (atomicAdd(a.tiles + Hkv, 1u) == gridDim.x - 1) {
+            for (int i = 0; i < Hkv; ++i) atomicExch(a.tiles + i, 0u);
+            atomicExch(a.tiles + Hkv, 0u);
+        }
+    }
+    __syncthreads();
+    const int pick = s_pick;
+    if (pick < 0) return;
+    const int g = pick % Hkv;
+    const int tile = ntiles - 1 - pick / Hkv;        // heaviest tiles first
     const int t0 = tile * a.BT;
     const int t1 = min(t0 + a.BT, nR);
     const int off = a.R_off[a.layer];
@@ -471,7 +506,10 @@ void launch_one(const AttnArgs& a, bool bf16, int n_bound, hipStream_t st) {
     n_bound = n_bound > 0 ? n_bound : 1;                 // workgroup 0 still checks the count
     if (bf16) {
         const int ntiles = (n_bound + a.BT - 1) / a.BT;
-        hipLaunchKernelGGL((attn_bf16<D, FULL, kNW>), dim3(ntiles * a.Hkv), dim3(kNW * 64), 0, st, a);
+        const int nwg = ntiles * a.Hkv;
+        // One workgroup per tile of the bound plus an eighth spare (they exit
+        // once every counter is exhausted).
+        hipLaunchKernelGGL((attn_bf16<D, FULL, kNW>), dim3(nwg + nwg / 8), dim3(kNW * 64), 0, st, a);
     } else {
         hipLaunchKernelGGL((attn_f32<D, FULL>), dim3(n_bound, a.H), dim3(64), 0, st, a);
     }
@@ -504,6 +542,8 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.R_u = s.R_u;
     a.counts = s.counts;
     a.err = s.counts + p.L + 1;
+    a.tiles = s.tiles + ((size_t)(context_mode == RELAXKV_CONTEXT_FULL ? p.L : 0) + layer) *
+                            (size_t)(p.H_kv + 1);
     a.out = out;
     a.lse = lse_out;
     a.H = p.H;

@@ -24,7 +24,7 @@ bool dims_ok(const relaxkv_problem* p) {
 
 // Byte sizes of the set arrays, in carving order.
 struct SetsLayout {
-    size_t anchors, h, U, cidx, R_off, R_idx, R_u, src, rank, counts, edges, ctx, g, total;
+    size_t anchors, h, U, cidx, R_off, R_idx, R_u, src, rank, counts, edges, ctx, g, tiles, total;
 };
 
 SetsLayout sets_layout(const relaxkv_problem* p, int32_t k) {
@@ -43,8 +43,9 @@ SetsLayout sets_layout(const relaxkv_problem* p, int32_t k) {
     s.edges = align_up(2 * L * 8);
     s.ctx = align_up(L * T * 4);
     s.g = align_up(T * 4);
+    s.tiles = align_up(attn_tile_words(*p) * 4);
     s.total = s.anchors + s.h + s.U + s.cidx + s.R_off + s.R_idx + s.R_u + s.src + s.rank + s.counts +
-              s.edges + s.ctx + s.g;
+              s.edges + s.ctx + s.g + s.tiles;
     return s;
 }
 
@@ -52,7 +53,7 @@ bool sets_match(const relaxkv_problem* p, const relaxkv_sets* s) {
     return s && s->L == p->L && s->T_c == p->T_c &&
            s->k == relaxkv_anchor_count(p->anchor_ratio, p->T_c) && s->anchors && s->h &&
            s->U && s->cidx && s->R_off && s->R_idx && s->R_u && s->src && s->rank && s->counts &&
-           s->edges && s->ctx && s->g &&
+           s->edges && s->ctx && s->g && s->tiles &&
            s->context_sets >= RELAXKV_CONTEXT_SETS_UNION &&
            s->context_sets <= RELAXKV_CONTEXT_SETS_LAYERWISE;
 }
@@ -133,7 +134,8 @@ relaxkv_status relaxkv_sets_bind(const relaxkv_problem* p, void* dev_buf, size_t
     s.counts = (int32_t*)b; b += l.counts;
     s.edges = (int64_t*)b; b += l.edges;
     s.ctx = (int32_t*)b; b += l.ctx;
-    s.g = (float*)b;
+    s.g = (float*)b; b += l.g;
+    s.tiles = (uint32_t*)b;
     s.global_targets = 0;
     s.context_sets = RELAXKV_CONTEXT_SETS_UNION;
     *out = s;

@@ -29,9 +29,12 @@ namespace {
 constexpr int kSetThreads = 1024;
 constexpr int kSetPerThread = 8;
 
-__global__ void sets_reset(int32_t* __restrict__ h, int T, int32_t* __restrict__ rank, long n_rank) {
+__global__ void sets_reset(int32_t* __restrict__ h, int T, int32_t* __restrict__ rank, long n_rank,
+                           uint32_t* __restrict__ tiles, int n_tiles) {
     for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < T; i += gridDim.x * blockDim.x)
         h[i] = -1;
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n_tiles; i += gridDim.x * blockDim.x)
+        tiles[i] = 0u;
     for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_rank;
          i += (long)gridDim.x * blockDim.x)
         rank[i] = -1;
@@ -341,7 +344,7 @@ void launch_union(const relaxkv_problem& p, const relaxkv_sets& s, hipStream_t s
     const long n_rank = (long)L * T;
     const long rb = (n_rank + 255) / 256;
     hipLaunchKernelGGL(sets_reset, dim3(rb < 2048 ? (int)rb : 2048), dim3(256), 0, st, s.h, T,
-                       s.rank, n_rank);
+                       s.rank, n_rank, s.tiles, (int)attn_tile_words(p));
     const long nm = (long)L * s.k;
     const long mb = (nm + 255) / 256;
     hipLaunchKernelGGL(sets_mark, dim3(mb < 2048 ? (int)mb : 2048), dim3(256), 0, st, s.anchors,

@@ -52,7 +52,7 @@ class Sets(Structure):
                 ("anchors", c_void_p), ("h", c_void_p), ("U", c_void_p), ("cidx", c_void_p),
                 ("R_off", c_void_p), ("R_idx", c_void_p), ("R_u", c_void_p),
                 ("src", c_void_p), ("rank", c_void_p), ("counts", c_void_p),
-                ("edges", c_void_p), ("ctx", c_void_p), ("g", c_void_p),
+                ("edges", c_void_p), ("ctx", c_void_p), ("g", c_void_p), ("tiles", c_void_p),
                 ("global_targets", c_int32), ("context_sets", c_int32)]
 
 
@@ -399,6 +399,7 @@ class SetsBuffer:
         self.edges = view(s.edges, 2 * L, torch.int64)
         self.ctx = view(s.ctx, L * T, torch.int32).view(L, T)
         self.g = view(s.g, T, torch.float32)
+        self.tiles = view(s.tiles, 2 * L * (req.H_kv + 1), torch.int32).view(2, L, req.H_kv + 1)
 
     def counts_to_host(self, stream=None, check=True):
         """(counts [L+2], edges [2L]) on the host; synchronises the stream.  With

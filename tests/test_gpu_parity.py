@@ -362,3 +362,42 @@ def test_row_capacity_clamps_and_reports(gpu_lib, name):
     case.req.update_cache(case.sets, l, fresh[1], fresh[2], k_out, v_out)
     counts, _ = case.sets.counts_to_host()
     assert counts[case.L + 1] == 0
+
+
+def test_attention_tile_counters(gpu_lib):
+    """The bf16 attention's workgroups take their tiles from per-layer, per-mode
+    counters in the sets buffer: a set build zeroes every slot whatever the
+    buffer held, each launch returns its slot to zero, every target is computed
+    exactly once (outputs against the oracle on every target), and repeated
+    launches, interleaved across layers and modes on one stream, give the same
+    bits."""
+    w = SMALL["qwen-planted"]
+    case = Case(w)
+    a = synthetic_scores(case.L, case.T, seed=23)
+    sets_ref = oracle.build_sets(oracle.select(a.astype(np.float64), case.k), case.T)
+    case.sets.tiles.fill_(0x5A5A5A5A)
+    case.req.select(torch.from_numpy(a).cuda(), case.sets)
+    compare_sets(case.gpu_sets(), sets_ref)
+    assert case.sets.tiles.shape == (2, case.L, w.H_kv + 1)
+    assert int(case.sets.tiles.abs().sum()) == 0
+    layers = [0, 1, case.L - 1]
+    fresh = {l: case.fresh(l, sets_ref.R[l]) for l in layers}
+    first = {}
+    for rep in range(3):
+        for l in layers:
+            for mode, cm in (("union", relaxkv.CONTEXT_UNION), ("full", relaxkv.CONTEXT_FULL)):
+                n = len(sets_ref.R[l])
+                out = torch.empty(n, w.H, w.d, dtype=case.q.dtype, device="cuda")
+                lse = torch.empty(n, w.H, dtype=torch.float32, device="cuda")
+                case.req.sparse_attn(case.sets, l, *fresh[l], out, lse, context_mode=cm)
+                if rep == 0:
+                    first[(l, mode)] = (out, lse)
+                else:
+                    o0, s0 = first[(l, mode)]
+                    assert torch.equal(out, o0) and torch.equal(lse, s0), (rep, l, mode)
+        torch.cuda.synchronize()
+        assert int(case.sets.tiles.abs().sum()) == 0, rep
+    for (l, mode), (out, lse) in first.items():
+        O_ref, lse_ref = case.oracle_attn(l, sets_ref, fresh[l], mode=mode)
+        assert_close(out.float().cpu().numpy(), O_ref, w, f"O {mode} layer {l}", rel_gate=1e-2)
+        assert_close(lse.cpu().numpy(), lse_ref, w, f"lse {mode} layer {l}")

@@ -122,12 +122,12 @@ def test_sets_bind_carves_buffer(rk):
                                  ctypes.byref(s)) == 0
     assert (s.L, s.T_c, s.k) == (4, 2048, oracle_anchor_count(0.15, 2048))
     ptrs = [s.anchors, s.h, s.U, s.cidx, s.R_off, s.R_idx, s.R_u, s.src, s.rank, s.counts,
-            s.edges]
+            s.edges, s.ctx, s.g, s.tiles]
     assert ptrs[0] == base and ptrs == sorted(ptrs)
     assert all(x % 256 == 0 for x in ptrs)
     L, T, k = s.L, s.T_c, s.k
     sizes = [L * k * 4, T * 4, T * 4, T * 4, (L + 1) * 4, L * T * 4, L * T * 4, L * T * 4,
-             L * T * 4, (L + 2) * 4, 2 * L * 8]
+             L * T * 4, (L + 2) * 4, 2 * L * 8, L * T * 4, T * 4, 2 * L * (p.H_kv + 1) * 4]
     for a, b, n in zip(ptrs, ptrs[1:] + [base + nbytes], sizes):
         assert b - a >= n
     assert lib.relaxkv_sets_bind(ctypes.byref(p), ctypes.c_void_p(base), nbytes - 1,
