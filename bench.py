@@ -33,7 +33,7 @@ Other objects:
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--no-control] [--no-matched-targets] [--no-cpu-baseline]
-                       [--no-workloads]
+                       [--no-workloads] [--no-clock]
 """
 
 from __future__ import annotations
@@ -620,11 +620,13 @@ def held_clock(b: Bench, seconds=2.5):
     """Graphics clock of each XCD and socket power while the benchmark step runs.
 
     The device's metrics table (amdsmi) is sampled every 20 ms from a host thread
-    while whole steps run back to back for about `seconds`; clocks are the
-    median of the samples taken after the first 0.6 s (the table refreshes
-    about once a second), power is the energy counter's difference over the
-    run's wall time.  The attention holds the chip below its 2.4 GHz maximum,
-    so its fraction of the spec peak understates its use of the MFMA pipe."""
+    while whole steps run back to back for about `seconds`, after about 1.2 s of
+    steps that bring the clocks to their loaded state; clocks are the median of
+    the samples taken after the first 0.6 s (the table refreshes about once a
+    second).  Power is the energy counter's difference over the counter's own
+    timestamps (it too refreshes about once a second, so both readings fall in
+    busy time).  The attention holds the chip below its 2.4 GHz maximum, so its
+    fraction of the spec peak understates its use of the MFMA pipe."""
     import threading
     try:
         import amdsmi
@@ -648,8 +650,10 @@ def held_clock(b: Bench, seconds=2.5):
             samples.append((time.perf_counter(), clks or [], m.get("temperature_hotspot")))
             stop.wait(0.02)
 
-    b.step()
-    torch.cuda.synchronize()
+    tw = time.perf_counter()
+    while time.perf_counter() - tw < 1.2:
+        b.step()
+        torch.cuda.synchronize()
     try:
         e0 = amdsmi.amdsmi_get_energy_count(h)
     except Exception:                                        # noqa: BLE001
@@ -682,9 +686,11 @@ def held_clock(b: Bench, seconds=2.5):
                      "sampled while whole benchmark steps run back to back"}
     try:
         joules = (e1["energy_accumulator"] - e0["energy_accumulator"]) * e0["counter_resolution"] * 1e-6
-        if joules > 0:
-            res["socket_power_w"] = joules / (t1 - t0)
-            res["energy_j_per_step"] = joules / steps
+        span = (e1["timestamp"] - e0["timestamp"]) * 1e-9
+        if joules > 0 and span > 0.5:
+            res["socket_power_w"] = joules / span
+            res["energy_j_per_step"] = joules / span * (t1 - t0) / steps
+            res["energy_counter_span_s"] = span
     except Exception:                                        # noqa: BLE001
         pass
     return res
@@ -734,6 +740,8 @@ def main():
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip the other paper-shaped workloads (8K Llama-shaped, 16K "
                          "Qwen-shaped ratio sweep)")
+    ap.add_argument("--no-clock", action="store_true",
+                    help="skip sampling the clocks and power (amdsmi) while steps run")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run one plain device-to-device copy of MIB MiB (reference "
                          "kernel for scaling the HBM byte counters) and exit")
@@ -810,7 +818,7 @@ def main():
                      "frac_of_measured_gemm": attn_tflops / peaks["gemm_bf16_tflops"]},
         "measured_peaks": peaks,
     }
-    clk = held_clock(b)
+    clk = held_clock(b) if not args.no_clock else {"available": False, "reason": "--no-clock"}
     res["clock"] = clk
     if clk.get("available"):
         f = clk["gfxclk_mhz_mean"] / 2400.0
