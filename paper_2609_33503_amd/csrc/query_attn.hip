@@ -34,11 +34,16 @@ constexpr int kQaKeys = 64;            // keys per tile
 #ifndef RELAXKV_QA_WGS
 #define RELAXKV_QA_WGS 256                     // workgroups the key splits aim for (one per CU)
 #endif
+#ifndef QA_NH
+#define QA_NH 2
+#endif
 constexpr int kQaStages = RELAXKV_QA_STAGES;   // LDS ring depth (a K and a V tile per stage)
 constexpr int kQaMinSplit = 256;       // fewest cache keys per split
 constexpr int kQaMaxSplit = 4096;      // most cache keys per split
 constexpr int kQaRing = 4;             // K fragments read ahead of their MFMA
 constexpr float kQaSlack = 8.0f;       // log2 units the running max may lag the true max
+
+template <int N> struct Int { static constexpr int value = N; };
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -64,8 +69,9 @@ __device__ __forceinline__ float qa_pair_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
+template <int D, int NB, int NH>
+__global__ __launch_bounds__((NB + NH) * 64) void qattn_bf16(QaArgs a) {
+    constexpr int NW = NB + NH;            // waves: NB - NH whole row blocks, 2 NH half blocks
     constexpr int TK = kQaKeys;
     constexpr int KS = D / 16;             // k-steps of QK^T
     constexpr int DB = D / 32;             // 32-wide d blocks of O^T
@@ -91,9 +97,16 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
     const int ntq = split == a.n_split - 1 ? (a.Qn + TK - 1) / TK : 0;
     const int ntile = ntc + ntq;
 
+    // The wave's row block: waves below NB - NH own a whole block; the other
+    // 2 NH waves take the last NH blocks in halves (half 0: keys 0-31 of every
+    // tile, half 1: keys 32-63), so the waves of the four SIMDs carry equal work.
+    const int hw = w - (NB - NH);
+    const bool halfw = hw >= 0;
+    const int hsel = halfw ? hw / NH : 0;                 // the half this wave takes
+    const int blk = halfw ? NB - NH + hw % NH : w;
     // This lane's (token, head) row.  Within a tile, key index > lim is masked:
     // the cache tail of the split, or the causal future in the query tiles.
-    const int rho = (chunk * NW + w) * 32 + r32;
+    const int rho = (chunk * NB + blk) * 32 + r32;
     const bool valid = rho < a.n_rows;
     const int t_row = valid ? rho / a.G : 0;
     const int hh = valid ? rho - t_row * a.G : 0;
@@ -185,55 +198,47 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
     const int v_base0 = rl * ROWB | ((cl ^ tile_swz<D>(rl)) << 4) | ((lane & 1) << 3);
     const int v_base1 = (rl + 8) * ROWB | ((cl ^ tile_swz<D>(rl + 8)) << 4) | ((lane & 1) << 3);
 
-#pragma unroll
-    for (int tt = 0; tt < kQaStages - 1; ++tt)
-        if (tt < ntile) issue(tt);
-    for (int tt = 0; tt < ntile; ++tt) {
-        wait_tile(min(kQaStages - 2, ntile - 1 - tt));
-        if (tt + kQaStages - 1 < ntile) issue(tt + kQaStages - 1);
-        // Fragment byte addresses of this tile's ring stage: the stage (and the V
-        // tile base) only set bits above the swizzled chunk bits, so one add per
-        // tile and one xor per fragment address; made opaque per tile so they
-        // are recomputed rather than held in registers across the loop.
-        const char* kst = (const char*)Kt[0];
-        const uint32_t stage = (uint32_t)(tt % kQaStages) * (TK * D * 2);
-        const uint32_t vstage = lds_addr(Vt[0]) + stage;
-        int kbo = k_base + (int)stage;
-        uint32_t vb0 = v_base0 + vstage, vb1 = v_base1 + vstage;
+    // One tile for NKB 32-key blocks (2: the whole tile; 1: the wave's half,
+    // whose rows start hoff bytes into the tile and whose keys start at c0).
+    auto step = [&](auto nkb_t, const char* kst, uint32_t stage, uint32_t vstage, int c0, int lim,
+                    bool masked, uint32_t hoff) {
+        constexpr int NKB = decltype(nkb_t)::value;
+        int kbo = k_base + (int)stage + (int)hoff;
+        uint32_t vb0 = v_base0 + vstage + hoff, vb1 = v_base1 + vstage + hoff;
         asm volatile("" : "+v"(kbo), "+v"(vb0), "+v"(vb1));
-        const bool qt = tt >= ntc;
-        const int c0 = qt ? (tt - ntc) * TK : tt * TK;
-        const int lim = qt ? lim_q : nkc - 1;
         // S^T = K Q^T: s[kb][v] = S[row][key c0 + 32kb + 8(v/4) + 4hf + v%4]
-        f32x16 s[2] = {f32x16{}, f32x16{}};
-        auto frag = [&](int x) {                       // x = 2 ks + kb
-            return *(const bf16x8*)(kst + (x & 1) * 32 * ROWB + (kbo ^ ((x >> 1) << 5)));
+        f32x16 s[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) s[kb] = f32x16{};
+        auto frag = [&](int x) {                       // x = NKB ks + kb
+            return *(const bf16x8*)(kst + (x % NKB) * 32 * ROWB + (kbo ^ ((x / NKB) << 5)));
         };
         bf16x8 kf[kQaRing];
 #pragma unroll
         for (int i = 0; i < kQaRing; ++i) kf[i] = frag(i);
 #pragma unroll
-        for (int x = 0; x < 2 * KS; ++x) {
+        for (int x = 0; x < NKB * KS; ++x) {
             const bf16x8 cur = kf[x % kQaRing];
-            if (x + kQaRing < 2 * KS) kf[x % kQaRing] = frag(x + kQaRing);
-            s[x & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[x >> 1], s[x & 1], 0, 0, 0);
+            if (x + kQaRing < NKB * KS) kf[x % kQaRing] = frag(x + kQaRing);
+            s[x % NKB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur, qf[x / NKB], s[x % NKB], 0, 0, 0);
         }
-        if (qt || c0 + TK > nkc) {                     // cache tail or causal tile: mask
+        if (masked) {                                  // cache tail or causal tile
             const int e = lim - c0 - 4 * hf;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                if (8 * (v >> 2) + (v & 3) > e) s[0][v] = -INFINITY;
-                if (32 + 8 * (v >> 2) + (v & 3) > e) s[1][v] = -INFINITY;
-            }
-        }
-        // Two chains of 3-input maxima (two new values per instruction).
-        float m0 = fmaxf(s[0][0], s[0][1]), m1 = fmaxf(s[1][0], s[1][1]);
+            for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-        for (int v = 2; v < 16; v += 2) {
-            m0 = fmaxf(fmaxf(m0, s[0][v]), s[0][v + 1]);
-            m1 = fmaxf(fmaxf(m1, s[1][v]), s[1][v + 1]);
+                for (int v = 0; v < 16; ++v)
+                    if (32 * kb + 8 * (v >> 2) + (v & 3) > e) s[kb][v] = -INFINITY;
         }
-        const float mx = qa_pair_max(fmaxf(m0, m1)) * a.sl2;
+        // Chains of 3-input maxima (two new values per instruction).
+        float mk[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            mk[kb] = fmaxf(s[kb][0], s[kb][1]);
+#pragma unroll
+            for (int v = 2; v < 16; v += 2) mk[kb] = fmaxf(fmaxf(mk[kb], s[kb][v]), s[kb][v + 1]);
+        }
+        const float mx = qa_pair_max(NKB == 2 ? fmaxf(mk[0], mk[NKB - 1]) : mk[0]) * a.sl2;
         if (__any(mx > m_run + kQaSlack)) {
             const float m_new = mx > m_run + kQaSlack ? mx : m_run;
             const float alpha = fast_exp2(m_run - m_new);
@@ -244,9 +249,9 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
         }
         // The row sum adds the bf16 probabilities that the PV product uses, two
         // per dot2 instruction, in four chains.
-        bf16x8 pb[2][2];
+        bf16x8 pb[NKB][2];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 pb[kb][v >> 3][v & 7] = (__bf16)fast_exp2(fmaf(s[kb][v], a.sl2, -m_run));
@@ -255,7 +260,7 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
             const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
             float ls0 = 0.f, ls1 = 0.f, ls2 = 0.f, ls3 = 0.f;
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                 for (int k2 = 0; k2 < 2; ++k2) {
                     const bf16x8 q8 = pb[kb][k2];
@@ -268,7 +273,7 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
         }
         // O^T += V^T P^T
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
             for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -282,9 +287,66 @@ __global__ __launch_bounds__(NW * 64) void qattn_bf16(QaArgs a) {
                         bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
                     o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pb[kb][k2], o[db], 0, 0, 0);
                 }
-    }
+    };
 
-    const float l_tot = qa_pair_sum(l_run);
+#pragma unroll
+    for (int tt = 0; tt < kQaStages - 1; ++tt)
+        if (tt < ntile) issue(tt);
+    // The tile loop, once per wave kind (so each is allocated on its own).
+    auto run = [&](auto nkb_t) {
+        constexpr int NKB = decltype(nkb_t)::value;
+        for (int tt = 0; tt < ntile; ++tt) {
+            wait_tile(min(kQaStages - 2, ntile - 1 - tt));
+            if (tt + kQaStages - 1 < ntile) issue(tt + kQaStages - 1);
+            const char* kst = (const char*)Kt[0];
+            const uint32_t stage = (uint32_t)(tt % kQaStages) * (TK * D * 2);
+            const uint32_t vstage = lds_addr(Vt[0]) + stage;
+            const bool qt = tt >= ntc;
+            const int c0 = qt ? (tt - ntc) * TK : tt * TK;
+            const int lim = qt ? lim_q : nkc - 1;
+            if (NKB == 1)
+                step(nkb_t, kst, stage, vstage, c0 + 32 * hsel, lim, qt || c0 + TK > nkc,
+                     (uint32_t)hsel * (32 * ROWB));
+            else
+                step(nkb_t, kst, stage, vstage, c0, lim, qt || c0 + TK > nkc, 0u);
+        }
+    };
+    if (NH > 0 && halfw) run(Int<1>{});
+    else run(Int<2>{});
+
+    float l_tot = qa_pair_sum(l_run);
+    if constexpr (NH > 0) {
+        // The half-1 wave of each split block hands (O, m, l) to its half-0 wave
+        // through LDS (the ring is free once every wave is past the last tile);
+        // the half-0 wave combines them like two key splits.
+        float* mo = (float*)&Kt[0][0];                     // [NH][DB * 16][64]
+        float* ml = mo + NH * DB * 16 * 64;                // [NH][2][64]
+        __syncthreads();
+        const int pr = hw % NH;
+        if (halfw && hsel == 1) {
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) mo[((pr * DB + db) * 16 + v) * 64 + lane] = o[db][v];
+            ml[(pr * 2) * 64 + lane] = m_run;
+            ml[(pr * 2 + 1) * 64 + lane] = l_tot;
+        }
+        __syncthreads();
+        if (halfw && hsel == 1) return;
+        if (halfw) {
+            const float mB = ml[(pr * 2) * 64 + lane], lB = ml[(pr * 2 + 1) * 64 + lane];
+            const float m = fmaxf(m_run, mB);
+            const float wA = m_run == -INFINITY ? 0.f : fast_exp2(m_run - m);
+            const float wB = mB == -INFINITY ? 0.f : fast_exp2(mB - m);
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    o[db][v] = o[db][v] * wA + mo[((pr * DB + db) * 16 + v) * 64 + lane] * wB;
+            l_tot = l_tot * wA + lB * wB;
+            m_run = m;
+        }
+    }
     if (!valid) return;
     const float inv = 1.0f / l_tot;
     const size_t prow = ((size_t)split * a.Hkv + g) * a.rows_pad + rho;
@@ -416,10 +478,10 @@ int qa_waves(int rows_pad) {
     return nrb <= 4 ? 4 : (nrb <= 8 || nrb > 10) ? 8 : 10;
 }
 
-template <int D, int NW>
+template <int D, int NB, int NH>
 void launch_qattn_bf16(const QaArgs& a, int n_chunks, hipStream_t st, void* out, float* lse) {
-    hipLaunchKernelGGL((qattn_bf16<D, NW>), dim3(a.n_split, a.Hkv, n_chunks), dim3(NW * 64), 0, st,
-                       a);
+    hipLaunchKernelGGL((qattn_bf16<D, NB, NH>), dim3(a.n_split, a.Hkv, n_chunks),
+                       dim3((NB + NH) * 64), 0, st, a);
     hipLaunchKernelGGL((qattn_merge<D>), dim3(a.Qn * a.H), dim3(D), 0, st,
                        (const uint16_t*)a.part_o, (const float*)a.part_l, a.n_split, a.Hkv, a.G,
                        a.H, a.rows_pad, (uint16_t*)out, lse);
@@ -496,14 +558,16 @@ hipError_t launch_query_attn(const relaxkv_problem& p, int layer, const void* k_
     a.sl2 = scale * kLog2e;
     const int nw = qa_waves(w.rows_pad);
     const int n_chunks = w.n_chunks;
+    // Ten row blocks run as 12 waves (two blocks in key halves), so that each of the
+    // four SIMDs carries two and a half blocks.
     if (p.d == 128) {
-        if (nw == 4) launch_qattn_bf16<128, 4>(a, n_chunks, st, out, lse_out);
-        else if (nw == 8) launch_qattn_bf16<128, 8>(a, n_chunks, st, out, lse_out);
-        else launch_qattn_bf16<128, 10>(a, n_chunks, st, out, lse_out);
+        if (nw == 4) launch_qattn_bf16<128, 4, 0>(a, n_chunks, st, out, lse_out);
+        else if (nw == 8) launch_qattn_bf16<128, 8, 0>(a, n_chunks, st, out, lse_out);
+        else launch_qattn_bf16<128, 10, QA_NH>(a, n_chunks, st, out, lse_out);
     } else {
-        if (nw == 4) launch_qattn_bf16<64, 4>(a, n_chunks, st, out, lse_out);
-        else if (nw == 8) launch_qattn_bf16<64, 8>(a, n_chunks, st, out, lse_out);
-        else launch_qattn_bf16<64, 10>(a, n_chunks, st, out, lse_out);
+        if (nw == 4) launch_qattn_bf16<64, 4, 0>(a, n_chunks, st, out, lse_out);
+        else if (nw == 8) launch_qattn_bf16<64, 8, 0>(a, n_chunks, st, out, lse_out);
+        else launch_qattn_bf16<64, 10, QA_NH>(a, n_chunks, st, out, lse_out);
     }
     return hipGetLastError();
 }
