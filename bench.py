@@ -12,7 +12,7 @@ including scoring, selection and set construction.  ms_per_step / L is the
 per-layer time.  The "roofline" object covers the dominant kernel
 (sparse-context attention), timed with HIP events on the launch stream, with
 its fraction of the published bf16 peak and of the rate a plain bf16 GEMM
-reaches in the same process ("measured_peaks": a device copy and a GEMM).
+reaches in the same process ("measured_peaks": a device copy, a read-only sum and a GEMM).
 Other objects:
 - "scoring": both scoring modes, and the one-pass chain in which the
   library's query-side completion produces the row LSE the scorer takes;
@@ -337,9 +337,10 @@ def time_one_pass_scoring(b: Bench, reps=5):
 
 def measured_peaks():
     """Rates this GPU reaches on plain library work, measured in this process:
-    a 2 GiB device copy (read + write bytes) and a 8192^3 bf16 GEMM (rocBLAS /
-    hipBLASLt through torch).  The fractions against them sit next to the
-    fractions against the published peaks."""
+    a 2 GiB device copy (read + write bytes), an int64 sum over 4 GiB (read
+    only) and a 8192^3 bf16 GEMM (rocBLAS / hipBLASLt through torch).  The
+    fractions against them sit next to the fractions against the published
+    peaks."""
     n = 2 << 30
     src = torch.empty(n, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)
@@ -353,7 +354,21 @@ def measured_peaks():
     e1.record()
     torch.cuda.synchronize()
     copy_gbs = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del src, dst
+    # read-only: an int64 sum over 4 GiB (the read-only torch kernel that came
+    # closest to the HBM peak: fp32 sums issue-bind near 4 TB/s)
+    del dst
+    big = torch.empty(2 * n, dtype=torch.uint8, device="cuda").view(torch.int64)
+    big.zero_()
+    big.sum()
+    torch.cuda.synchronize()
+    e0, e1 = mk(), mk()
+    e0.record()
+    for _ in range(5):
+        big.sum()
+    e1.record()
+    torch.cuda.synchronize()
+    read_gbs = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, big
     m = 8192
     a = torch.randn(m, m, dtype=torch.bfloat16, device="cuda")
     bm = torch.randn(m, m, dtype=torch.bfloat16, device="cuda")
@@ -368,8 +383,9 @@ def measured_peaks():
     gemm = 2.0 * m ** 3 * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12
     del a, bm, c
     torch.cuda.empty_cache()
-    return {"copy_gbs": copy_gbs, "gemm_bf16_tflops": gemm,
-            "note": "2 GiB device copy (read + write bytes) and a 8192^3 bf16 torch GEMM"}
+    return {"copy_gbs": copy_gbs, "read_gbs": read_gbs, "gemm_bf16_tflops": gemm,
+            "note": "2 GiB device copy (read + write bytes), an int64 sum over 4 GiB (read "
+                    "only) and a 8192^3 bf16 torch GEMM"}
 
 
 def _input_digest(t, chunk=1 << 26):
@@ -781,6 +797,8 @@ def main():
                                       "(its row LSE) then relaxkv_score with that q_lse")
     scoring["self_contained_frac_of_measured_copy"] = scoring["self_contained_gbs"] / peaks["copy_gbs"]
     scoring["supplied_lse_frac_of_measured_copy"] = scoring["supplied_lse_gbs"] / peaks["copy_gbs"]
+    scoring["supplied_lse_frac_of_measured_read"] = scoring["supplied_lse_gbs"] / peaks["read_gbs"]
+    scoring["self_contained_frac_of_measured_read"] = scoring["self_contained_gbs"] / peaks["read_gbs"]
     res = {
         "metric": "repair-attention TFLOP/s + ms/layer, 14B-shaped layer, 32K ctx, 15% anchors",
         "value": tflops,
@@ -835,6 +853,7 @@ def main():
         res["context_variants"] = time_context_variants(b)
         res["query_attn"] = time_query_attn(b)
         res["query_attn"]["frac_of_measured_copy"] = res["query_attn"]["gbs"] / peaks["copy_gbs"]
+        res["query_attn"]["frac_of_measured_read"] = res["query_attn"]["gbs"] / peaks["read_gbs"]
     if not args.no_cpu_baseline:
         res["anchor_jaccard_gpu_vs_oracle_scores"] = anchor_jaccard(b)
     if not args.no_control:
