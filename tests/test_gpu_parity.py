@@ -35,6 +35,10 @@ SMALL = {
     "long-query": synth.shrink(W["qwen14b-16k"], L=2, T_c=1300, Qn=100),
     "gqa16": synth.shrink(W["llama8b-8k"], L=2, T_c=900, H=32, H_kv=2, Qn=8),
     "gqa12-d64": synth.shrink(W["llama8b-8k"], L=3, T_c=1100, H=24, H_kv=2, d=64, Qn=12),
+    # more KV heads than XCDs, and a KV-head count that does not divide their number:
+    # the attention's per-head tile counters start workgroups on every head
+    "kv16": synth.shrink(W["llama8b-8k"], L=2, T_c=1000, H=32, H_kv=16, Qn=8),
+    "kv3": synth.shrink(W["llama8b-8k"], L=2, T_c=1000, H=12, H_kv=3, Qn=8),
 }
 
 
