@@ -38,9 +38,17 @@
  *   float32) for Q/K/V and attention outputs.
  * - Layers are 0-based; positions are context positions 0 .. T_c-1 (the
  *   query tokens are never targets or context).
- * - The library keeps no state between calls and calls are reentrant; two
- *   calls that write the same buffers must be ordered by the caller.  The one
- *   piece of request state on the host is in relaxkv_sets: the set-building
+ * - The library keeps no host state between calls and calls are reentrant;
+ *   two calls that write the same buffers must be ordered by the caller.
+ *   Device state lives in caller-owned buffers: the sets buffer holds the bf16
+ *   attention's work counters (each launch returns its slot to zero), so two
+ *   relaxkv_sparse_attn launches with the same sets, layer and context mode
+ *   must not overlap in time; relaxkv_query_attn_noalloc uses a device array
+ *   of the library instead (see there).
+ * - Compute calls enqueue kernels only (no allocation, memset or host
+ *   synchronisation; relaxkv_counts_to_host is the one synchronising call),
+ *   so a sequence of them can be captured into a HIP graph and replayed.
+ * - The one piece of request state on the host is in relaxkv_sets: the set-building
  *   calls record in it which kind of target and context lists they built
  *   (global_targets, context_sets), so pass the struct the last of them
  *   filled, not an older copy.  A stale copy cannot make a kernel overrun:
