@@ -21,3 +21,16 @@ def gpu_lib():
         pytest.fail("GPU test collected on a machine without a GPU")
     from paper_2609_33503_amd import relaxkv
     return relaxkv.load()
+
+
+@pytest.fixture(scope="session")
+def rk():
+    """The binding with the in-tree library loaded for host-only calls (built
+    first when it is missing or stale; CPU tests never launch kernels)."""
+    from paper_2609_33503_amd import build, relaxkv
+    try:
+        build.verify()
+    except RuntimeError:                             # missing or stale: build it (CPU only)
+        build.build()
+    relaxkv.load()
+    return relaxkv

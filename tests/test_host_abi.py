@@ -17,17 +17,6 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "relaxkv.h")
 
 
-@pytest.fixture(scope="module")
-def rk():
-    from paper_2609_33503_amd import build, relaxkv
-    try:
-        build.verify()
-    except RuntimeError:                             # missing or stale: build it (CPU only)
-        build.build()
-    relaxkv.load()
-    return relaxkv
-
-
 def _declared():
     txt = open(HEADER).read()
     decl = r"^(?:const char\*|int32_t|size_t|relaxkv_status)\s+(relaxkv_[a-z_]+)\("
