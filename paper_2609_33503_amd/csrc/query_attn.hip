@@ -5,10 +5,14 @@
 //
 // bf16 path, split over keys (the row set is small: n_query * G rows per KV
 // head against T_c keys):
-// - a workgroup owns one KV head g, one chunk of up to NW*32 (token, head) rows
-//   (token t, head g*G + hh -> row t*G + hh) and one split of consecutive
-//   cache keys (sized on the host so that one round of workgroups covers the
-//   layer); the last split also takes the query tokens' own keys;
+// - a workgroup owns one KV head g, one chunk of up to NB 32-row blocks of
+//   (token, head) rows (token t, head g*G + hh -> row t*G + hh) and one split
+//   of consecutive cache keys (sized on the host so that one round of
+//   workgroups covers the layer); the last split also takes the query tokens'
+//   own keys;
+// - ten blocks run as twelve waves (two blocks in key halves whose partial
+//   results are combined through LDS at the end), so the four SIMDs of a CU
+//   (waves w and w+4 share one) carry equal work;
 // - K and V tiles of 64 keys stream into a 4-deep ring of swizzled LDS buffers
 //   by direct global->LDS loads (see tile_swz), three tiles ahead of the MFMAs;
 // - each wave computes S^T = K Q^T for its 32 rows (one row per lane), a
