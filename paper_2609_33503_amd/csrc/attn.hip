@@ -146,6 +146,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
         s_pick = pick;
         __threadfence();
         if (atomicAdd(a.tiles + Hkv, 1u) == gridDim.x - 1) {
+            __threadfence();                       // every other pick happens before the resets
             for (int i = 0; i < Hkv; ++i) atomicExch(a.tiles + i, 0u);
             atomicExch(a.tiles + Hkv, 0u);
         }
