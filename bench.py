@@ -31,7 +31,7 @@ Other objects:
   its MFMA and exp2 issue bounds next to the HBM bound;
 - "cpu_baseline": the float64 oracle, stage by stage, on this host's cores.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+Usage: python bench.py [--gpus 1] [--steps K (20)] [--warmup W (1)] [--workload NAME]
                        [--no-control] [--no-matched-targets] [--no-cpu-baseline]
                        [--no-workloads] [--no-clock]
 """
@@ -155,11 +155,20 @@ class Bench:
         select_ms = np.mean([e["s1"].elapsed_time(e["s2"]) for e in evs])
         sets_ms = np.mean([e["s2"].elapsed_time(e["s3"]) for e in evs])
         attn = np.array([[a.elapsed_time(b) for a, b in e["a"]] for e in evs])   # [steps][L]
+        step_ms = np.array([e["s0"].elapsed_time(e["a"][-1][1]) for e in evs])    # per step
+        attn_step = attn.sum(axis=1)
         return dict(wall_s=wall, ms_per_step=1e3 * wall / steps, score_ms=float(score_ms),
                     select_ms=float(select_ms), sets_ms=float(sets_ms),
                     attn_ms_per_layer=attn.mean(axis=0).tolist(),
-                    attn_ms_total=float(attn.sum(axis=1).mean()),
-                    attn_launch_ms_avg=float(attn.mean()))
+                    attn_ms_total=float(attn_step.mean()),
+                    attn_launch_ms_avg=float(attn.mean()),
+                    step_ms_events={"mean": float(step_ms.mean()),
+                                    "median": float(np.median(step_ms)),
+                                    "min": float(step_ms.min()), "max": float(step_ms.max())},
+                    attn_ms_all_layers_events={"mean": float(attn_step.mean()),
+                                               "median": float(np.median(attn_step)),
+                                               "min": float(attn_step.min()),
+                                               "max": float(attn_step.max())})
 
 
 def time_cache_update(b: Bench, reps=3):
@@ -742,7 +751,7 @@ def scoring_report(w, ms_two_pass, ms_one_pass):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="qwen14b-32k-planted", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--no-control", action="store_true",
@@ -818,6 +827,12 @@ def main():
                    "chunk_tokens": w.chunk, "query_tokens": w.Qn, "q_heads": w.H,
                    "kv_heads": w.H_kv, "head_dim": w.d, "anchor_ratio": w.ratio,
                    "k": b.req.k},
+        "timing": {"protocol": f"{args.warmup} warm-up step(s), then {args.steps} timed steps, "
+                               f"each cycling all {w.L} layers; value and ms_per_step from the "
+                               "wall clock between synchronisations, the rest from HIP events "
+                               "on the library's stream",
+                   "step_ms": r["step_ms_events"],
+                   "attn_ms_all_layers": r["attn_ms_all_layers_events"]},
         "stages_ms": {"score": r["score_ms"], "select": r["select_ms"],
                       "build_sets": r["sets_ms"], "sparse_attn_all_layers": r["attn_ms_total"]},
         "ms_per_layer_by_stage": {"score": r["score_ms"] / w.L, "select": r["select_ms"] / w.L,
