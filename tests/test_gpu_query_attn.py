@@ -24,6 +24,10 @@ SMALL = {
     "d64-bf16": synth.shrink(W["llama8b-8k"], L=2, T_c=777, H=8, H_kv=2, d=64, Qn=24),
     "mha-bf16": synth.shrink(W["llama8b-8k"], L=2, T_c=640, H=4, H_kv=4, Qn=8),
     "big-group": synth.shrink(W["llama8b-8k"], L=2, T_c=900, H=32, H_kv=2, Qn=40),   # 640 rows
+    # 288 rows (nine 32-row blocks: the twelve-wave kernel with a padding block among
+    # its key-half waves) and 320 rows at d = 64 (the twelve-wave kernel's d = 64 form)
+    "rows288": synth.shrink(W["llama8b-8k"], L=2, T_c=1100, Qn=72),
+    "rows320-d64": synth.shrink(W["qwen14b-16k"], L=2, T_c=1000, d=64),
     "fp32-d128": synth.shrink(W["tiny-2L-1k-fp32"], L=2, T_c=300, d=128, H=6, H_kv=3, Qn=5),
 }
 
