@@ -245,6 +245,29 @@ def test_full_size_attention_sampled(big_case, mode):
         assert np.exp(s - float(lse[t, 0])).sum() == pytest.approx(1.0, abs=2e-3)
 
 
+def test_full_size_update_cache_bit_exact(big_case):
+    """The cache update at 32K in the benchmark's launch configuration: the
+    repaired layers equal the oracle's bit for bit (out of place), and layers
+    that were not updated are untouched."""
+    a = synthetic_scores(BIG.L, BIG.T_c, seed=5)
+    sets_ref = oracle.build_sets(oracle.select(a.astype(np.float64), big_case.k), BIG.T_c)
+    big_case.req.select(torch.from_numpy(a).cuda(), big_case.sets)
+    compare_sets(big_case.gpu_sets(), sets_ref)
+    k_out, v_out = big_case.kc.clone(), big_case.vc.clone()
+    layers = (0, 19, BIG.L - 1)
+    for l in layers:
+        _, kn, vn = big_case.fresh(l, sets_ref.R[l])
+        big_case.req.update_cache(big_case.sets, l, kn, vn, k_out, v_out)
+        torch.cuda.synchronize()
+        kr, vr = oracle.update_cache(l, sets_ref, synth.to_f64(kn), synth.to_f64(vn),
+                                     synth.to_f64(big_case.kc[l]), synth.to_f64(big_case.vc[l]))
+        assert np.array_equal(synth.to_f64(k_out[l]), kr), l
+        assert np.array_equal(synth.to_f64(v_out[l]), vr), l
+    others = [l for l in range(BIG.L) if l not in layers]
+    assert torch.equal(k_out[others], big_case.kc[others])
+    assert torch.equal(v_out[others], big_case.vc[others])
+
+
 def _mixed_context(kc_l, vc_l, fresh_k, fresh_v, ctx, rank):
     """fp32 K~/V~ [H_kv][|ctx|][d] over the positions ctx: the fresh row of a
     position with rank >= 0, its cached row otherwise."""
