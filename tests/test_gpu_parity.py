@@ -341,19 +341,22 @@ def test_full_size_attention_every_target(big_case, mode):
 @pytest.mark.parametrize("name,ratio", [("llama8b-8k", None), ("qwen14b-16k", 0.05),
                                         ("qwen14b-16k", 0.15), ("qwen14b-16k", 0.30)])
 def test_full_size_workloads(gpu_lib, name, ratio):
-    """Full-size workloads on sampled layers: scores within tolerance; selection
-    and sets bit-exact on the oracle's fp32 scores of those layers (the other
-    layers take seeded scores); attention on sampled targets of each sampled
-    layer, in the launch configuration the benchmark uses."""
+    """Full-size workloads: scores within tolerance on every layer (on sampled
+    layers for the 16K ratio points other than 0.15, whose scores are the same);
+    selection and sets bit-exact on the oracle's fp32 scores of those layers (the
+    other layers take seeded scores); attention on sampled targets of three
+    layers, in the launch configuration the benchmark uses."""
     w = W[name]
     case = Case(w, ratio=ratio)
     L, T = case.L, case.T
     layers = [0, L // 2, L - 1]
+    score_layers = list(range(L)) if ratio in (None, 0.15) else layers
     a_gpu = case.gpu_scores().cpu().numpy()
-    a_ref, _, _ = case.oracle_scores(layers)
-    assert_close(a_gpu[layers], a_ref, w, f"scores {name}")
     a = synthetic_scores(L, T, seed=21)
-    a[layers] = a_ref.astype(np.float32)
+    for l in score_layers:                           # one layer at a time (float64 copies)
+        a_ref, _, _ = case.oracle_scores([l])
+        assert_close(a_gpu[[l]], a_ref, w, f"scores {name} layer {l}")
+        a[l] = a_ref[0].astype(np.float32)
     anchors = case.gpu_select(torch.from_numpy(a).cuda())
     anchors_ref = oracle.select(a.astype(np.float64), case.k)
     assert np.array_equal(anchors, anchors_ref)
