@@ -94,9 +94,13 @@ typedef int32_t relaxkv_status;
 #define RELAXKV_CONTEXT_SETS_GLOBAL    1  /* U_l = TopK(g, |U|) for every layer (Global Sparse) */
 #define RELAXKV_CONTEXT_SETS_LAYERWISE 2  /* U_l = TopK(a_l, |U|) per layer (Layerwise Sparse) */
 
-/* Limits of this build (checked by relaxkv_validate). */
+/* Limits of this build (checked by relaxkv_validate).  The bf16 path also
+ * needs one layer's cache slab, T_c * H_kv * d elements, below
+ * RELAXKV_MAX_BF16_LAYER_ELEMS (its attention addresses rows with 32-bit
+ * element offsets); larger bf16 problems get RELAXKV_EUNSUPPORTED. */
 #define RELAXKV_MAX_LAYERS 1024
 #define RELAXKV_MAX_TC     (1 << 22)
+#define RELAXKV_MAX_BF16_LAYER_ELEMS ((int64_t)1 << 31)
 
 /*
  * The problem every call describes.
@@ -195,7 +199,10 @@ const char* relaxkv_status_string(relaxkv_status s);
  * r is not a finite number in [0, 1] or T_c < 1. */
 int32_t relaxkv_anchor_count(double anchor_ratio, int32_t T_c);
 
-/* Host only.  Checks dimensions, pointers, dtype and the ratio of `p`. */
+/* Host only.  Checks dimensions, pointers, dtype and the ratio of `p`:
+ * RELAXKV_EINVAL for a bad dimension, pointer, scale or ratio,
+ * RELAXKV_EUNSUPPORTED for a head_dim, dtype, GQA group or bf16 layer size
+ * (see the limits above) this build has no kernel for. */
 relaxkv_status relaxkv_validate(const relaxkv_problem* p);
 
 /* Host only.  Device scratch bytes relaxkv_score needs (0 when p is invalid). */

@@ -67,17 +67,17 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
                               int n_rows, void* out, float* lse_out, int context_mode,
                               hipStream_t st);
 
-// Rows an attention or cache-update launch may process for layer `layer`: the
-// caller's row capacity, and the bound on |R_l| of the lists the sets hold
-// (min(T_c, (L - l) k) for RelaxKV's targets: R_l lies in the union of S_l'
-// for l' >= l; T_c for a global target list).  Kernels clamp the device count
-// to it and set RELAXKV_ERR_ROWS when they have to.
 // Words of relaxkv_sets::tiles: per context mode and layer, one next-tile
 // counter per KV head and one workgroup count.
 inline size_t attn_tile_words(const relaxkv_problem& p) {
     return 2 * (size_t)p.L * (size_t)(p.H_kv + 1);
 }
 
+// Rows an attention or cache-update launch may process for layer `layer`: the
+// caller's row capacity, and the bound on |R_l| of the lists the sets hold
+// (min(T_c, (L - l) k) for RelaxKV's targets: R_l lies in the union of S_l'
+// for l' >= l; T_c for a global target list).  Kernels clamp the device count
+// to it and set RELAXKV_ERR_ROWS when they have to.
 inline int row_cap(const relaxkv_problem& p, const relaxkv_sets& s, int layer, int n_rows) {
     const long kb = s.global_targets ? (long)p.T_c : (long)(p.L - layer) * s.k;
     long cap = kb < p.T_c ? kb : p.T_c;

@@ -95,6 +95,11 @@ relaxkv_status relaxkv_validate(const relaxkv_problem* p) {
     if (p->d != 64 && p->d != 128) return RELAXKV_EUNSUPPORTED;
     // The bf16 attention tile packs whole GQA groups into kAttnRows rows.
     if (p->dtype == RELAXKV_DTYPE_BF16 && p->H / p->H_kv > kAttnRows) return RELAXKV_EUNSUPPORTED;
+    // The bf16 attention's fills address fresh and cached rows with 32-bit
+    // element offsets (below T_c * H_kv * d).
+    if (p->dtype == RELAXKV_DTYPE_BF16 &&
+        (int64_t)p->T_c * p->H_kv * p->d >= RELAXKV_MAX_BF16_LAYER_ELEMS)
+        return RELAXKV_EUNSUPPORTED;
     return RELAXKV_OK;
 }
 

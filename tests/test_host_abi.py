@@ -77,6 +77,10 @@ def _problem(rk, **kw):
     ({"H": 512, "H_kv": 1}, -3),                      # a GQA group wider than the bf16 tile
     ({"H": 512, "H_kv": 1, "dtype": 0}, 0),           # fp32 kernels have no such limit
     ({"d": 64, "dtype": 0}, 0),
+    # one layer's bf16 cache slab must stay below 2^31 elements (32-bit row offsets)
+    ({"L": 1, "T_c": 1 << 21, "H": 8, "H_kv": 8}, -3),
+    ({"L": 1, "T_c": (1 << 21) - 1, "H": 8, "H_kv": 8}, 0),
+    ({"L": 1, "T_c": 1 << 21, "H": 8, "H_kv": 8, "dtype": 0}, 0),
 ])
 def test_validate(rk, kw, status):
     p = _problem(rk, **kw)
