@@ -309,39 +309,92 @@ def time_query_attn(b: Bench, reps=3):
             "tflops": 4.0 * w.H * w.d * w.Qn * (w.T_c + (w.Qn + 1) / 2) / (us * 1e-6) / 1e12}
 
 
-def time_one_pass_scoring(b: Bench, reps=5):
+class OnePass:
     """The one-pass scoring pipeline as the library runs it: the query-side
     completion (relaxkv_query_attn over the naive cache, per layer) produces
     each query row's log-sum-exp, which relaxkv_score then takes as q_lse and
-    reads K once.  Times the score call alone and the whole chain."""
-    w = b.w
-    lse = torch.empty(w.L, w.Qn, w.H, dtype=torch.float32, device="cuda")
-    kvq = [synth.make_query_kv(w, l, "cuda") for l in range(w.L)]
-    qa_out = torch.empty(w.Qn, w.H, w.d, dtype=b.q.dtype, device="cuda")
-    qws = b.req.alloc_query_workspace()
-    req = relaxkv.Request(b.q, b.kc, b.vc, w.ratio, q_lse=lse)
-    ws = req.alloc_workspace()
-    out = torch.empty_like(b.scores)
+    reads K once."""
 
-    def chain():
-        for l in range(w.L):
-            b.req.query_attn(l, b.kc, b.vc, *kvq[l], qa_out, lse[l], qws)
-        req.score(ws, out)
+    def __init__(self, b: Bench):
+        w = self.w = b.w
+        self.b = b
+        self.lse = torch.empty(w.L, w.Qn, w.H, dtype=torch.float32, device="cuda")
+        self.kvq = [synth.make_query_kv(w, l, "cuda") for l in range(w.L)]
+        self.qa_out = torch.empty(w.Qn, w.H, w.d, dtype=b.q.dtype, device="cuda")
+        self.qws = b.req.alloc_query_workspace()
+        self.req = relaxkv.Request(b.q, b.kc, b.vc, w.ratio, q_lse=self.lse)
+        self.ws = self.req.alloc_workspace()
+        self.out = torch.empty_like(b.scores)
+        self.chain()                     # warm
+        torch.cuda.synchronize()
 
-    chain()
-    torch.cuda.synchronize()
+    def query_attn_all(self):
+        for l in range(self.w.L):
+            self.b.req.query_attn(l, self.b.kc, self.b.vc, *self.kvq[l], self.qa_out,
+                                  self.lse[l], self.qws)
+
+    def score(self):
+        self.req.score(self.ws, self.out)
+
+    def chain(self):
+        self.query_attn_all()
+        self.score()
+
+
+def time_one_pass_scoring(op: OnePass, reps=5):
+    """Times the one-pass score call alone and the whole chain."""
     mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     e0, e1, e2, e3 = mk(), mk(), mk(), mk()
     e0.record()
     for _ in range(reps):
-        req.score(ws, out)
+        op.score()
     e1.record()
     e2.record()
     for _ in range(reps):
-        chain()
+        op.chain()
     e3.record()
     torch.cuda.synchronize()
     return {"score_ms": e0.elapsed_time(e1) / reps, "chain_ms": e2.elapsed_time(e3) / reps}
+
+
+class _Repeat:
+    """A call repeated n times per step (the clock sampler runs steps)."""
+
+    def __init__(self, fn, n):
+        self.fn, self.n = fn, n
+
+    def step(self):
+        for _ in range(self.n):
+            self.fn()
+
+
+def power_by_call(b: Bench, op: OnePass, seconds=2.0):
+    """Clock and socket power while one kind of call runs back to back, and the
+    call's time in that state (HIP events over 20 calls right after the
+    sampling).  Every kernel of the path runs at the socket power limit, so
+    each settles at its own clock: this is the clock its issue bounds scale
+    with."""
+    out = {}
+    for name, fn, n in (("score_supplied_lse", op.score, 20),
+                        ("score_self_contained", lambda: b.req.score(b.ws, b.scores), 10),
+                        ("query_attn_all_layers", op.query_attn_all, 5)):
+        c = held_clock(_Repeat(fn, n), seconds=seconds)
+        if not c.get("available"):
+            return {"available": False, "reason": c.get("reason")}
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(20):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = {"ms_per_call": e0.elapsed_time(e1) / 20,
+                     "gfxclk_mhz_mean": c["gfxclk_mhz_mean"],
+                     "gfxclk_mhz_by_xcd": c["gfxclk_mhz_by_xcd"],
+                     "socket_power_w": c.get("socket_power_w")}
+    out["available"] = True
+    out["note"] = ("each call repeated back to back for about 3 s (amdsmi clocks and energy "
+                   "counter), then timed over 20 calls; the socket limit is 1400 W")
+    return out
 
 
 def measured_peaks():
@@ -798,7 +851,8 @@ def main():
     attn_tflops = flops / (r["attn_ms_total"] * 1e-3) / 1e12
     bf16 = w.dtype == "bf16"
     peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
-    one_pass = time_one_pass_scoring(b)
+    op = OnePass(b)
+    one_pass = time_one_pass_scoring(op)
     peaks = measured_peaks()
     scoring = scoring_report(w, r["score_ms"], one_pass["score_ms"])
     scoring["one_pass_chain_ms"] = one_pass["chain_ms"]
@@ -862,6 +916,18 @@ def main():
             k: (v if k == "hbm_us" else v / f) for k, v in bnd.items()}
         if "energy_j_per_step" in clk:
             clk["tflop_per_joule"] = flops / 1e12 / clk["energy_j_per_step"]
+        pw = power_by_call(b, op)
+        res["power_by_call"] = pw
+        if pw.get("available"):
+            # The supplied-LSE pass against its issue bounds at the clock it holds.
+            s1 = pw["score_supplied_lse"]
+            fs = s1["gfxclk_mhz_mean"] / 2400.0
+            us = 1e3 * s1["ms_per_call"] / w.L
+            scoring["supplied_lse_at_its_held_clock"] = {
+                "us_per_layer": us, "gfxclk_mhz": s1["gfxclk_mhz_mean"],
+                "mfma_floor_us": bnd["mfma_us_one_pass"] / fs,
+                "exp2_floor_us": bnd["exp2_us_one_pass"] / fs,
+                "frac_of_mfma_floor": bnd["mfma_us_one_pass"] / fs / us}
     res["cache_update"] = time_cache_update(b)
     if not args.no_matched_targets:
         res["matched_targets"] = time_matched_targets(b)
