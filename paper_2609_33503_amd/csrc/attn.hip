@@ -7,9 +7,11 @@
 //
 // bf16 kernel (bf16 MFMA 32x32x16, fp32 accumulation, flash-style online
 // softmax in the exp2 domain):
-// - a workgroup of NW = 12 waves owns NW*32 (target, head) rows of one KV head
-//   g: floor(NW*32/G) consecutive targets times the G query heads that share g,
-//   so every K/V row brought into LDS is used by all G heads of NW*32/G targets;
+// - a workgroup of NW = 12 waves owns NW*32 consecutive (target, head) rows of
+//   one KV head g (row t*G + hh: target t, the hh-th of the G query heads that
+//   share g), so every K/V row brought into LDS is used by NW*32 rows; a tile
+//   may begin or end inside a target's group of heads, so no row is idle when
+//   G does not divide NW*32;
 // - context keys go in steps of 64 through a 4-deep ring of LDS buffers (a K
 //   and a V tile per step, unpadded rows with an XOR swizzle), filled by direct
 //   global->LDS loads that choose per key between the fresh rows
@@ -57,7 +59,7 @@ struct AttnArgs {
     uint32_t* tiles;         // this layer's and mode's work counters: [Hkv] next tile, [Hkv] workgroups
     void* out;
     float* lse;
-    int H, Hkv, G, T, layer, BT;
+    int H, Hkv, G, T, layer;
     int cap;                 // rows this launch may process (row capacity, host bound)
     float scale;             // softmax scale (natural units)
 };
@@ -122,7 +124,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     const int nR_dev = a.counts[1 + a.layer];
     const int nR = min(nR_dev, a.cap);
     if (nR_dev > a.cap && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(a.err, RELAXKV_ERR_ROWS);
-    const int ntiles = (nR + a.BT - 1) / a.BT;
+    constexpr int TR = NW * 32;            // (target, head) rows per tile
+    const int nrows = nR * a.G;            // rows of one KV head (< 2^31: T_c <= 2^22, G <= TR)
+    const int ntiles = (nrows + TR - 1) / TR;
     // Tile choice.  Each KV head's tiles are handed out heaviest first from its
     // counter; a workgroup starts with a head tied to its XCD (so the
     // workgroups of one XCD share that head's K/V in their L2) and moves on to
@@ -156,8 +160,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     if (pick < 0) return;
     const int g = pick % Hkv;
     const int tile = ntiles - 1 - pick / Hkv;        // heaviest tiles first
-    const int t0 = tile * a.BT;
-    const int t1 = min(t0 + a.BT, nR);
+    const int r0 = tile * TR;                        // the tile's rows [r0, r1)
+    const int r1 = min(r0 + TR, nrows);
+    const int t0 = r0 / a.G, t1 = (r1 - 1) / a.G + 1;  // the targets they belong to
     const int off = a.R_off[a.layer];
     const int32_t* lim_of = FULL ? a.R_idx + off : a.R_u + off;
     const int cmin = lim_of[t0];
@@ -168,17 +173,16 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     const int r32 = lane & 31, hf = lane >> 5;
     const float sl2 = a.scale * kLog2e;
 
-    const int rho = w * 32 + r32;
-    const int tl = rho / a.G, hh = rho - tl * a.G;
-    const int t_row = t0 + tl;
-    const bool valid = tl < a.BT && t_row < t1;
-    const int lim_v = lim_of[valid ? t_row : t0];   // value select: no pointer to cmax
+    const int row = r0 + w * 32 + r32;
+    const bool valid = row < r1;
+    const int t_row = valid ? row / a.G : t0;
+    const int hh = valid ? row - t_row * a.G : 0;
+    const int lim_v = lim_of[t_row];                 // value select: no pointer to cmax
     const int lim = valid ? lim_v : cmax;
     const int head = g * a.G + hh;
     bf16x8 qf[KS];
     {
-        const uint16_t* qrow = (const uint16_t*)a.q_new +
-                               ((size_t)(valid ? t_row : t0) * a.H + (valid ? head : 0)) * D;
+        const uint16_t* qrow = (const uint16_t*)a.q_new + ((size_t)t_row * a.H + head) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qrow + ks * 16 + hf * 8);
         // Consumed here, so the compiler's waits for these loads stay before the
@@ -506,7 +510,8 @@ template <int D, bool FULL>
 void launch_one(const AttnArgs& a, bool bf16, int n_bound, hipStream_t st) {
     n_bound = n_bound > 0 ? n_bound : 1;                 // workgroup 0 still checks the count
     if (bf16) {
-        const int ntiles = (n_bound + a.BT - 1) / a.BT;
+        const long rows = (long)n_bound * a.G;
+        const int ntiles = (int)((rows + kAttnRows - 1) / kAttnRows);
         const int nwg = ntiles * a.Hkv;
         // One workgroup per tile of the bound plus an eighth spare (they exit
         // once every counter is exhausted).
@@ -552,7 +557,6 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
     a.G = p.H / p.H_kv;
     a.T = p.T_c;
     a.layer = layer;
-    a.BT = bf16 ? kAttnRows / a.G : 1;
     a.scale = p.softmax_scale > 0.f ? p.softmax_scale : 1.0f / sqrtf((float)p.d);
     // The grid covers the row cap; the device count (clamped to it) decides
     // which workgroups run.

@@ -93,7 +93,8 @@ relaxkv_status relaxkv_validate(const relaxkv_problem* p) {
     if (p->dtype != RELAXKV_DTYPE_F32 && p->dtype != RELAXKV_DTYPE_BF16)
         return RELAXKV_EUNSUPPORTED;
     if (p->d != 64 && p->d != 128) return RELAXKV_EUNSUPPORTED;
-    // The bf16 attention tile packs whole GQA groups into kAttnRows rows.
+    // The bf16 attention counts (target, head) rows of a KV head in 32-bit
+    // integers: |R_l| * G < 2^22 * kAttnRows < 2^31.
     if (p->dtype == RELAXKV_DTYPE_BF16 && p->H / p->H_kv > kAttnRows) return RELAXKV_EUNSUPPORTED;
     // The bf16 attention's fills address fresh and cached rows with 32-bit
     // element offsets (below T_c * H_kv * d).
