@@ -179,6 +179,10 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     const int hh = valid ? row - t_row * a.G : 0;
     const int lim_v = lim_of[t_row];                 // value select: no pointer to cmax
     const int lim = valid ? lim_v : cmax;
+    // The largest limit among the wave's rows (limits ascend with the row), -1
+    // for a wave without rows: steps past it are masked for every row of the wave.
+    const int w_first = r0 + w * 32, w_last = min(w_first + 31, r1 - 1);
+    const int wlim = __builtin_amdgcn_readfirstlane(w_last < w_first ? -1 : lim_of[w_last / a.G]);
     const int head = g * a.G + hh;
     bf16x8 qf[KS];
     {
@@ -278,6 +282,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
         else wait_loads_barrier<0>();
         if (j + NST < S) issue_idx(j + NST);
         if (j + NST - 1 < S) issue_rows(j + NST - 1);
+        // A step whose keys all lie past every limit of the wave's rows adds
+        // exact zeros to them (p = 0): the wave only keeps the ring moving.
+        if (j * TK > wlim) continue;
         // S^T = K Q^T: s[kb][v] = S[row][key 64 j + 32 kb + 8(v/4) + 4 hf + v%4]
         f32x16 s[2];
         {

@@ -3,7 +3,8 @@
 Each case plants one mistake in a copy of the oracle's source (a dropped
 scale, a flipped tie-break, an off-by-one causal limit, a fresh/cached swap,
 ...), loads the copy as a module of its own, points the pin tests of
-test_oracle_pins at it, and requires at least one of the named pins to fail.
+test_oracle_pins at it, and requires the case's first named pin (a
+deterministic one) to fail.
 The oracle itself is never modified; every planted mistake must match its
 site in the source exactly once, so an edit of the oracle cannot turn a case
 into a silent no-op.  CPU only.
@@ -26,15 +27,15 @@ EXPORTS = ("anchor_count", "attention_flops", "build_sets", "build_sets_context"
            "build_sets_global", "global_scores", "global_scores_f32", "global_target_count",
            "query_attn", "score", "select", "select_global", "sparse_attn", "update_cache")
 
-# (name, text in the oracle, planted text, pins of which at least one must fail)
-# A pin is a test function of test_oracle_pins, or (function, kwargs).  The
-# first pin of every case is deterministic (no hypothesis draw), so a catch
-# never depends on which random examples a run happens to generate.
+# (name, text in the oracle, planted text, pins).  A pin is a test function of
+# test_oracle_pins, or (function, kwargs).  The first pin of every case is
+# deterministic (no hypothesis draw) and must fail; the others are further
+# pins that bear on the same definition (they run on the real oracle below).
 MUTANTS = [
     ("score: softmax scale dropped",
      "s = sigma * (q[l, :, h, :] @ k_cache[l, g].T)",
      "s = (q[l, :, h, :] @ k_cache[l, g].T)",
-     ["test_score_closed_form_logs", "test_score_matches_sdpa_attention_weights"]),
+     ["test_score_matches_sdpa_attention_weights", "test_score_closed_form_logs"]),
     ("score: query head h read against KV head h mod H_kv",
      "            g = h // G\n            s = sigma * (q[l, :, h, :]",
      "            g = h % H_kv\n            s = sigma * (q[l, :, h, :]",
@@ -86,7 +87,7 @@ MUTANTS = [
       ("test_attention_brute_force", dict(seed=0, L=3, T=40, k=6, mode="union"))]),
     ("sparse_attn: fresh values but cached keys",
      "    Kt[:, fresh, :] = np.transpose(k_new[rank[ctx_all[fresh]]], (1, 0, 2))\n", "",
-     ["test_hand_example_attention", "test_attention_full_union_is_causal_sdpa",
+     ["test_attention_full_union_is_causal_sdpa", "test_hand_example_attention",
       ("test_attention_brute_force", dict(seed=0, L=3, T=40, k=6, mode="union"))]),
     ("sparse_attn: query head h read against KV head h mod H_kv",
      "            g = h // G\n            s = sigma * (Kt[g, :m, :] @ q_new[t, h])",
@@ -95,8 +96,8 @@ MUTANTS = [
       ("test_attention_brute_force", dict(seed=0, L=3, T=40, k=6, mode="union"))]),
     ("sparse_attn: the full-prefix mode attends over the union",
      'ctx_all = np.arange(sets.T_c)', 'ctx_all = sets.context(layer)',
-     ["test_attention_full_union_is_causal_sdpa",
-      ("test_attention_brute_force", dict(seed=2, L=3, T=40, k=6, mode="full"))]),
+     [("test_attention_brute_force", dict(seed=2, L=3, T=40, k=6, mode="full")),
+      "test_attention_full_union_is_causal_sdpa"]),
     ("attention_flops: one product per edge instead of two",
      "return 4.0 * H * d * float(np.sum(edges))", "return 2.0 * H * d * float(np.sum(edges))",
      ["test_attention_flops_hand_example", "test_attention_flops_brute_force"]),
@@ -118,10 +119,8 @@ MUTANTS = [
     ("global_target_count: rounded instead of floored",
      "return min(int(np.floor(ratio * T_c)), int(n_union))",
      "return min(int(np.round(ratio * T_c)), int(n_union))",
-     [("test_global_target_count_floor_and_cap", dict(r=0.2, T=1000, nU=500, n=200)),
-      ("test_global_target_count_floor_and_cap", dict(r=0.15, T=1001, nU=999, n=150)),
-      ("test_global_target_count_floor_and_cap", dict(r=0.7, T=10, nU=10, n=7)),
-      ("test_global_target_count_floor_and_cap", dict(r=0.05, T=19, nU=19, n=0))]),
+     [("test_global_target_count_floor_and_cap", dict(r=0.05, T=19, nU=19, n=0)),
+      ("test_global_target_count_floor_and_cap", dict(r=0.2, T=1000, nU=500, n=200))]),
     ("global_target_count: not capped by |U|",
      "return min(int(np.floor(ratio * T_c)), int(n_union))",
      "return int(np.floor(ratio * T_c))",
@@ -139,13 +138,11 @@ MUTANTS = [
     ("build_sets_context: Global Sparse ranks by layer 0 instead of the layer mean",
      "shared = select_global(global_scores(a) if g is None else g, n)",
      "shared = select_global(a[0] if g is None else g, n)",
-     [("test_attention_context_variants_brute_force", dict(construction="global", mode="union")),
-      "test_build_sets_context_brute_force"]),
+     ["test_context_constructions_hand_example", "test_build_sets_context_brute_force"]),
     ("build_sets_context: Layerwise Sparse uses layer 0 for every layer",
      "ctx = [select(a[l:l + 1], n)[0] for l in range(L)]",
      "ctx = [select(a[0:1], n)[0] for l in range(L)]",
-     [("test_attention_context_variants_brute_force", dict(construction="layerwise", mode="union")),
-      "test_build_sets_context_brute_force"]),
+     ["test_context_constructions_hand_example", "test_build_sets_context_brute_force"]),
 ]
 
 
@@ -174,12 +171,11 @@ def test_pins_catch_planted_mistake(monkeypatch, name, old, new, catchers):
         monkeypatch.setattr(oracle, sym, getattr(mod, sym))      # `from oracle import` inside pins
         if hasattr(pins, sym):
             monkeypatch.setattr(pins, sym, getattr(mod, sym))    # names bound at import
-    for pin in catchers:
-        try:
-            _run(pin)
-        except Exception:            # the pin failed (an assertion, or an error inside the mutant)
-            return
-    pytest.fail(f"no pin caught the planted mistake {name!r} (tried {catchers})")
+    try:
+        _run(catchers[0])
+    except Exception:                # the pin failed (an assertion, or an error inside the mutant)
+        return
+    pytest.fail(f"the pin {catchers[0]} did not catch the planted mistake {name!r}")
 
 
 @pytest.mark.parametrize("pin", sorted({p if isinstance(p, str) else (p[0], tuple(sorted(p[1].items())))

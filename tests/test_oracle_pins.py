@@ -675,6 +675,29 @@ def test_build_sets_context_brute_force(L, T, seed, data, construction):
         assert s.edges.tolist() == base.edges.tolist()
 
 
+def test_context_constructions_hand_example():
+    # Worked by hand from the definitions (Sec. 4.4; ties to the lower position):
+    # a_0 = [1, 0, .7, 0, 0, 0], a_1 = [0, .9, 0, 0, 1, 0], k = 1 -> S_0 = {0},
+    # S_1 = {4}, U = {0, 4}, h = (0 at 0, 1 at 4), R_0 = {0, 4}, R_1 = {4}.
+    # Global Sparse: g = [.5, .45, .35, 0, .5, 0], top-2 = {0, 4} (0 and 4 tie at
+    # .5, both taken).  Layerwise Sparse: layer 0 top-2 of a_0 = {0, 2}; layer 1
+    # top-2 of a_1 = {1, 4}.  R_u = |U_l cap {j <= p}| - 1, src = rank in R_l.
+    from oracle import build_sets_context
+    a = np.array([[1, 0, 0.7, 0, 0, 0], [0, 0.9, 0, 0, 1, 0]])
+    S = np.array([[0], [4]])
+    g = build_sets_context(S, 6, a, "global")
+    assert [c.tolist() for c in g.ctx] == [[0, 4], [0, 4]]
+    assert [r.tolist() for r in g.R_u] == [[0, 1], [1]]
+    assert [x.tolist() for x in g.src] == [[0, 1], [-1, 0]]
+    assert g.edges.tolist() == [3, 2]
+    lw = build_sets_context(S, 6, a, "layerwise")
+    assert [c.tolist() for c in lw.ctx] == [[0, 2], [1, 4]]
+    assert [r.tolist() for r in lw.R_u] == [[0, 1], [1]]
+    assert [x.tolist() for x in lw.src] == [[0, -1], [-1, 0]]
+    assert lw.edges.tolist() == [3, 2]
+    assert [r.tolist() for r in lw.R] == [[0, 4], [4]] and lw.U.tolist() == [0, 4]
+
+
 def test_context_global_equals_layerwise_for_identical_layers():
     from oracle import build_sets_context
     rng = np.random.default_rng(24)
