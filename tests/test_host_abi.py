@@ -87,6 +87,23 @@ def test_validate(rk, kw, status):
     assert rk.load().relaxkv_validate(ctypes.byref(p)) == status
 
 
+@pytest.mark.parametrize("kw,n_split", [
+    # one round of 256 workgroups: 256 / H_kv splits of at least 256 keys (at 32K, 40q/8kv:
+    # 32 splits of 1024 keys; the GPU test shape "many-splits" takes 34)
+    (dict(T_c=32768, H=40, H_kv=8, n_query=64), 32),
+    (dict(T_c=8500, H=4, H_kv=2, n_query=8), 34),
+    (dict(T_c=1500, H=32, H_kv=8, n_query=64), 6),
+])
+def test_query_workspace_split_count(rk, kw, n_split):
+    p = _problem(rk, L=1, **kw)
+    G = kw["H"] // kw["H_kv"]
+    rows_pad = (kw["n_query"] * G + 31) // 32 * 32
+    rows = n_split * kw["H_kv"] * rows_pad
+    al = lambda x: (x + 255) // 256 * 256          # noqa: E731
+    assert rk.load().relaxkv_query_attn_workspace_bytes(ctypes.byref(p)) == \
+        al(rows * 128 * 2) + al(rows * 4)
+
+
 def test_validate_null(rk):
     assert rk.load().relaxkv_validate(None) == rk.EINVAL
 
