@@ -39,6 +39,10 @@ SMALL = {
     # the attention's per-head tile counters start workgroups on every head
     "kv16": synth.shrink(W["llama8b-8k"], L=2, T_c=1000, H=32, H_kv=16, Qn=8),
     "kv3": synth.shrink(W["llama8b-8k"], L=2, T_c=1000, H=12, H_kv=3, Qn=8),
+    # G = 7 and G = 10 do not divide the 384 rows of an attention tile: tiles begin and
+    # end inside a target's group of heads, whose context two workgroups then read
+    "gqa7": synth.shrink(W["llama8b-8k"], L=3, T_c=1200, H=14, H_kv=2, Qn=8),
+    "gqa10-d64": synth.shrink(W["llama8b-8k"], L=2, T_c=1000, H=20, H_kv=2, d=64, Qn=8),
 }
 
 
