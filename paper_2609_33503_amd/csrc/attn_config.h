@@ -19,7 +19,8 @@ namespace relaxkv {
 #ifndef RELAXKV_ATTN_LEAN
 #define RELAXKV_ATTN_LEAN 1         // 3-input max chains and bf16 dot2 row sums in the softmax
 #endif
-// (target, head) rows per workgroup: a GQA group of G heads must fit.
+// (target, head) rows per workgroup (the bf16 path takes GQA groups of at most
+// this many heads, which keeps its row counts below 2^31).
 constexpr int kAttnRows = RELAXKV_ATTN_WAVES * 32;
 
 }  // namespace relaxkv
