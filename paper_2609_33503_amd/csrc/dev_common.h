@@ -127,6 +127,10 @@ __device__ __forceinline__ void wait_loads_barrier() {
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(lds_void*)p;
 }
+// M0 is reserved to the compiler, which ignores it in a clobber list: these
+// helpers are only used in kernels that contain no compiler-generated use of
+// M0 (on gfx950 LDS instructions do not read it), so the value they leave in
+// M0 cannot reach another instruction.
 __device__ __forceinline__ void fill_lds16(const void* src, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                  :: "v"(src), "s"(lds) : "memory", "m0");

@@ -104,10 +104,11 @@ __global__ __launch_bounds__((NB + NH) * 64) void qattn_bf16(QaArgs a) {
     // The wave's row block: waves below NB - NH own a whole block; the other
     // 2 NH waves take the last NH blocks in halves (half 0: keys 0-31 of every
     // tile, half 1: keys 32-63), so the waves of the four SIMDs carry equal work.
+    constexpr int NHD = NH > 0 ? NH : 1;   // (no half waves when NH = 0: halfw is never true)
     const int hw = w - (NB - NH);
     const bool halfw = hw >= 0;
-    const int hsel = halfw ? hw / NH : 0;                 // the half this wave takes
-    const int blk = halfw ? NB - NH + hw % NH : w;
+    const int hsel = halfw ? hw / NHD : 0;                // the half this wave takes
+    const int blk = halfw ? NB - NH + hw % NHD : w;
     // This lane's (token, head) row.  Within a tile, key index > lim is masked:
     // the cache tail of the split, or the causal future in the query tiles.
     const int rho = (chunk * NB + blk) * 32 + r32;

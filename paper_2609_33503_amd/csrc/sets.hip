@@ -308,7 +308,7 @@ __global__ __launch_bounds__(kSetThreads) void ctx_layers(
     const int32_t* __restrict__ ctx, int ctx_stride, int T, const int32_t* __restrict__ R_off,
     const int32_t* __restrict__ R_idx, const int32_t* __restrict__ counts,
     const int32_t* __restrict__ rank, int32_t* __restrict__ R_u, int32_t* __restrict__ src,
-    int64_t* __restrict__ edges, int L) {
+    int64_t* __restrict__ edges) {
     __shared__ long long red[kSetThreads / 64];
     const int l = blockIdx.x, tid = threadIdx.x;
     const int32_t* ctx_l = ctx + (size_t)l * ctx_stride;
@@ -370,7 +370,7 @@ hipError_t launch_build_sets_context(const relaxkv_problem& p, const float* scor
     if (e != hipSuccess) return e;
     const int stride = construction == RELAXKV_CONTEXT_SETS_GLOBAL ? 0 : T;
     hipLaunchKernelGGL(ctx_layers, dim3(L), dim3(kSetThreads), 0, st, (const int32_t*)s.ctx, stride,
-                       T, s.R_off, s.R_idx, s.counts, s.rank, s.R_u, s.src, s.edges, L);
+                       T, s.R_off, s.R_idx, s.counts, s.rank, s.R_u, s.src, s.edges);
     return hipGetLastError();
 }
 
