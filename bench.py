@@ -341,20 +341,23 @@ class OnePass:
         self.score()
 
 
-def time_one_pass_scoring(op: OnePass, reps=5):
-    """Times the one-pass score call alone and the whole chain."""
+def time_one_pass_scoring(op: OnePass, reps=20, warm=3):
+    """Times the one-pass score call alone (mean of `reps` calls after `warm`
+    untimed ones) and the whole chain."""
     mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     e0, e1, e2, e3 = mk(), mk(), mk(), mk()
+    for _ in range(warm):
+        op.score()
     e0.record()
     for _ in range(reps):
         op.score()
     e1.record()
     e2.record()
-    for _ in range(reps):
+    for _ in range(5):
         op.chain()
     e3.record()
     torch.cuda.synchronize()
-    return {"score_ms": e0.elapsed_time(e1) / reps, "chain_ms": e2.elapsed_time(e3) / reps}
+    return {"score_ms": e0.elapsed_time(e1) / reps, "chain_ms": e2.elapsed_time(e3) / 5}
 
 
 class _Repeat:
