@@ -376,6 +376,7 @@ __global__ __launch_bounds__((NB + NH) * 64) void qattn_bf16(QaArgs a) {
 // weights are staged in LDS; each thread then sums its d element with several
 // partial loads in flight.
 constexpr int kQaMergeSplits = 1024;   // splits per LDS pass
+constexpr int kQaFixedSplits = 32;     // split count with its own merge kernel
 
 template <int D>
 __global__ __launch_bounds__(D) void qattn_merge(const uint16_t* __restrict__ part_o,
@@ -421,6 +422,49 @@ __global__ __launch_bounds__(D) void qattn_merge(const uint16_t* __restrict__ pa
             z += wl[s];
             acc = fmaf(wl[s], bf16_bits_to_f32(part_o[((s0 + s) * stride + row0) * D + e]), acc);
         }
+    }
+    out[(size_t)th * D + e] = f32_to_bf16_bits(acc / z);
+    if (lse && e == 0) lse[th] = (M + __log2f(z)) * kLn2;
+}
+
+// The same combination for exactly NS splits (the split count one round of
+// workgroups gives at 8 KV heads): every split's partial element and its
+// log-sum-exp are loaded before any of them is used, with no predication, so
+// a thread waits for memory once instead of once per batch.  Same operations
+// in the same order as qattn_merge, so the results are the same bits.
+template <int D, int NS>
+__global__ __launch_bounds__(D) void qattn_merge_fixed(const uint16_t* __restrict__ part_o,
+                                                       const float* __restrict__ part_l,
+                                                       int Hkv, int G, int H, int rows_pad,
+                                                       uint16_t* __restrict__ out,
+                                                       float* __restrict__ lse) {
+    static_assert(NS <= 64, "one wave holds the splits' log-sum-exps");
+    __shared__ float wl[NS];
+    __shared__ float red[D / 64];
+    const int th = blockIdx.x;                      // t * H + h
+    const int t = th / H, h = th - t * H;
+    const int g = h / G, rho = t * G + (h - g * G);
+    const int e = threadIdx.x;
+    const size_t stride = (size_t)Hkv * rows_pad;   // between splits
+    const uint16_t* po = part_o + ((size_t)g * rows_pad + rho) * D + e;
+    uint16_t raw[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) raw[s] = po[s * stride * D];
+    const int el = e < NS ? e : NS - 1;
+    const float ls = part_l[el * stride + (size_t)g * rows_pad + rho];
+    float M = wave_max(e < NS ? ls : -INFINITY);
+    if ((e & 63) == 0) red[e >> 6] = M;
+    __syncthreads();
+    M = red[0];
+#pragma unroll
+    for (int i = 1; i < D / 64; ++i) M = fmaxf(M, red[i]);
+    if (e < NS) wl[e] = fast_exp2(ls - M);
+    __syncthreads();
+    float z = 0.f, acc = 0.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        z += wl[s];
+        acc = fmaf(wl[s], bf16_bits_to_f32(raw[s]), acc);
     }
     out[(size_t)th * D + e] = f32_to_bf16_bits(acc / z);
     if (lse && e == 0) lse[th] = (M + __log2f(z)) * kLn2;
@@ -487,9 +531,14 @@ template <int D, int NB, int NH>
 void launch_qattn_bf16(const QaArgs& a, int n_chunks, hipStream_t st, void* out, float* lse) {
     hipLaunchKernelGGL((qattn_bf16<D, NB, NH>), dim3(a.n_split, a.Hkv, n_chunks),
                        dim3((NB + NH) * 64), 0, st, a);
-    hipLaunchKernelGGL((qattn_merge<D>), dim3(a.Qn * a.H), dim3(D), 0, st,
-                       (const uint16_t*)a.part_o, (const float*)a.part_l, a.n_split, a.Hkv, a.G,
-                       a.H, a.rows_pad, (uint16_t*)out, lse);
+    if (a.n_split == kQaFixedSplits)
+        hipLaunchKernelGGL((qattn_merge_fixed<D, kQaFixedSplits>), dim3(a.Qn * a.H), dim3(D), 0, st,
+                           (const uint16_t*)a.part_o, (const float*)a.part_l, a.Hkv, a.G, a.H,
+                           a.rows_pad, (uint16_t*)out, lse);
+    else
+        hipLaunchKernelGGL((qattn_merge<D>), dim3(a.Qn * a.H), dim3(D), 0, st,
+                           (const uint16_t*)a.part_o, (const float*)a.part_l, a.n_split, a.Hkv,
+                           a.G, a.H, a.rows_pad, (uint16_t*)out, lse);
 }
 
 }  // namespace

@@ -29,7 +29,8 @@ SMALL = {
     "rows288": synth.shrink(W["llama8b-8k"], L=2, T_c=1100, Qn=72),
     "rows320-d64": synth.shrink(W["qwen14b-16k"], L=2, T_c=1000, d=64),
     "fp32-d128": synth.shrink(W["tiny-2L-1k-fp32"], L=2, T_c=300, d=128, H=6, H_kv=3, Qn=5),
-    # 34 key splits (of 256 keys): more splits than any other shape here
+    # 32 key splits (the merge kernel for exactly 32) and 34 (the general merge)
+    "splits32": synth.shrink(W["llama8b-8k"], L=1, T_c=8192, Qn=8),
     "many-splits": synth.shrink(W["llama8b-8k"], L=1, T_c=8500, H=4, H_kv=2, Qn=8),
 }
 

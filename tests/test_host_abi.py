@@ -89,9 +89,11 @@ def test_validate(rk, kw, status):
 
 @pytest.mark.parametrize("kw,n_split", [
     # one round of 256 workgroups: 256 / H_kv splits of at least 256 keys (at 32K, 40q/8kv:
-    # 32 splits of 1024 keys; the GPU test shape "many-splits" takes 34)
+    # 32 splits of 1024 keys, which have a merge kernel of their own; the GPU test shapes
+    # "splits32" and "many-splits" take 32 and 34)
     (dict(T_c=32768, H=40, H_kv=8, n_query=64), 32),
     (dict(T_c=8500, H=4, H_kv=2, n_query=8), 34),
+    (dict(T_c=8192, H=32, H_kv=8, n_query=8), 32),
     (dict(T_c=1500, H=32, H_kv=8, n_query=64), 6),
 ])
 def test_query_workspace_split_count(rk, kw, n_split):
