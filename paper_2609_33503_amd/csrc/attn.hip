@@ -23,7 +23,8 @@
 //   the lane 32 away; P^T stays in registers as the B operand of
 //   O^T = V^T P^T, whose V^T operand comes from transposing LDS reads;
 // - the mask is the staircase of the targets' limits: steps below the first
-//   target's limit run unmasked, the rest compare each key with its row's limit;
+//   target's limit run unmasked, the rest compare each key with its row's limit,
+//   and a wave skips the arithmetic of steps past all of its rows' limits;
 // - tiles are taken heaviest-first (the last targets have the longest
 //   contexts) from per-KV-head counters; a workgroup starts with the head tied
 //   to its XCD, so the workgroups of one XCD share a KV head and its L2
