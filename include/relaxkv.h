@@ -338,8 +338,8 @@ relaxkv_status relaxkv_build_sets_global(const relaxkv_problem* p, relaxkv_sets*
  * holds) the surplus targets are not computed and RELAXKV_ERR_ROWS is set in
  * the error word, so no row past the caller's buffers is read or written.  The
  * naive cache of the layer is read from p->k_cache / p->v_cache.  A target
- * whose context is empty (only with relaxkv_build_sets_global, union context)
- * gets O = 0 and lse = -inf.
+ * whose context is empty (only with the lists of relaxkv_build_sets_global or
+ * relaxkv_build_sets_context, union context) gets O = 0 and lse = -inf.
  * The bf16 kernel's workgroups take their tiles from the s->tiles slot of this
  * layer and context mode (dynamic balancing across XCDs whose clocks differ):
  * two launches with the same sets, layer and context mode must not overlap in
