@@ -285,10 +285,12 @@ def _mixed_context(kc_l, vc_l, fresh_k, fresh_v, ctx, rank):
     return K.contiguous(), V.contiguous()
 
 
-@pytest.mark.parametrize("mode", ["union", "full"])
-def test_full_size_attention_every_target(big_case, mode):
-    """Every target and head of one 32K layer (|R_l| about 27 500 targets x 40
-    heads), in the benchmark's launch configuration: the kernel's log-sum-exp
+@pytest.mark.parametrize("mode,l", [("union", 19), ("full", 19), ("union", 39)])
+def test_full_size_attention_every_target(big_case, mode, l):
+    """Every target and head of a 32K layer (|R_l| about 27 500 targets x 40
+    heads at layer 19; the 4 915 targets of the last layer, the sparsest in U,
+    where tiles span the widest staircase and waves skip the most steps), in
+    the benchmark's launch configuration: the kernel's log-sum-exp
     normalises the softmax of its own context (sum_j exp(s_j - lse) = 1) and its
     output is the softmax-weighted sum of the context rows under that
     normaliser.  A property check at full size, recomputed in fp32 from the
@@ -301,7 +303,6 @@ def test_full_size_attention_every_target(big_case, mode):
     big_case.req.select(torch.from_numpy(a).cuda(), big_case.sets)
     compare_sets(big_case.gpu_sets(), sets_ref)
     cm = relaxkv.CONTEXT_FULL if mode == "full" else relaxkv.CONTEXT_UNION
-    l = 19
     R_l = np.asarray(sets_ref.R[l])
     n = len(R_l)
     fresh = big_case.fresh(l, R_l)
