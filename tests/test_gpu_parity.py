@@ -78,7 +78,7 @@ def test_pipeline_small(gpu_lib, name):
     _pipeline(Case(SMALL[name]))
 
 
-@pytest.mark.parametrize("name", ["tiny", "qwen-planted", "qwen-latent"])
+@pytest.mark.parametrize("name", ["tiny", "qwen-planted", "qwen-latent", "gqa7", "d64-bf16", "mha-bf16"])
 def test_full_prefix_small(gpu_lib, name):
     _pipeline(Case(SMALL[name]), mode="full")
 
