@@ -505,3 +505,45 @@ def test_attention_tile_counters(gpu_lib):
         O_ref, lse_ref = case.oracle_attn(l, sets_ref, fresh[l], mode=mode)
         assert_close(out.float().cpu().numpy(), O_ref, w, f"O {mode} layer {l}", rel_gate=1e-2)
         assert_close(lse.cpu().numpy(), lse_ref, w, f"lse {mode} layer {l}")
+
+
+def test_attention_concurrent_layers_and_modes(gpu_lib):
+    """Launches for different layers, and for the two context modes of one
+    layer, may run at the same time (each takes its tiles from its own counter
+    slot): three launches on three streams with no ordering between them give
+    the bits of the same launches run one after another, and every slot is back
+    at zero afterwards."""
+    w = SMALL["qwen-planted"]
+    case = Case(w)
+    a = synthetic_scores(case.L, case.T, seed=29)
+    sets_ref = oracle.build_sets(oracle.select(a.astype(np.float64), case.k), case.T)
+    case.req.select(torch.from_numpy(a).cuda(), case.sets)
+    compare_sets(case.gpu_sets(), sets_ref)
+    jobs = [(0, relaxkv.CONTEXT_UNION), (1, relaxkv.CONTEXT_UNION), (0, relaxkv.CONTEXT_FULL),
+            (case.L - 1, relaxkv.CONTEXT_FULL)]
+    fresh = {l: case.fresh(l, sets_ref.R[l]) for l, _ in jobs}
+
+    def buffers():
+        return {j: (torch.empty(len(sets_ref.R[j[0]]), w.H, w.d, dtype=case.q.dtype, device="cuda"),
+                    torch.empty(len(sets_ref.R[j[0]]), w.H, dtype=torch.float32, device="cuda"))
+                for j in jobs}
+
+    seq = buffers()
+    for (l, cm), (out, lse) in seq.items():
+        case.req.sparse_attn(case.sets, l, *fresh[l], out, lse, context_mode=cm)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in jobs]
+    for rep in range(3):
+        con = buffers()
+        torch.cuda.synchronize()
+        for s, ((l, cm), (out, lse)) in zip(streams, con.items()):
+            case.req.sparse_attn(case.sets, l, *fresh[l], out, lse, context_mode=cm, stream=s)
+        torch.cuda.synchronize()
+        for j in jobs:
+            assert torch.equal(con[j][0], seq[j][0]) and torch.equal(con[j][1], seq[j][1]), (rep, j)
+        assert int(case.sets.tiles.abs().sum()) == 0, rep
+    for (l, cm), (out, lse) in seq.items():
+        mode = "full" if cm == relaxkv.CONTEXT_FULL else "union"
+        O_ref, lse_ref = case.oracle_attn(l, sets_ref, fresh[l], mode=mode)
+        assert_close(out.float().cpu().numpy(), O_ref, w, f"O {mode} layer {l}", rel_gate=1e-2)
+        assert_close(lse.cpu().numpy(), lse_ref, w, f"lse {mode} layer {l}")
