@@ -285,28 +285,18 @@ def _mixed_context(kc_l, vc_l, fresh_k, fresh_v, ctx, rank):
     return K.contiguous(), V.contiguous()
 
 
-@pytest.mark.parametrize("mode,l", [("union", 19), ("full", 19), ("union", 39)])
-def test_full_size_attention_every_target(big_case, mode, l):
-    """Every target and head of a 32K layer (|R_l| about 27 500 targets x 40
-    heads at layer 19; the 4 915 targets of the last layer, the sparsest in U,
-    where tiles span the widest staircase and waves skip the most steps), in
-    the benchmark's launch configuration: the kernel's log-sum-exp
-    normalises the softmax of its own context (sum_j exp(s_j - lse) = 1) and its
-    output is the softmax-weighted sum of the context rows under that
-    normaliser.  A property check at full size, recomputed in fp32 from the
-    same bf16 inputs; the element-wise parity with the oracle is the sampled
-    test above."""
-    w = BIG
-    a = synthetic_scores(w.L, w.T_c, seed=5)
-    anchors_ref = oracle.select(a.astype(np.float64), big_case.k)
-    sets_ref = oracle.build_sets(anchors_ref, w.T_c)
-    big_case.req.select(torch.from_numpy(a).cuda(), big_case.sets)
-    compare_sets(big_case.gpu_sets(), sets_ref)
+def _every_target_property(case, sets_ref, l, mode):
+    """Every target and head of layer l in the benchmark's launch configuration:
+    the kernel's log-sum-exp normalises the softmax of its own context
+    (sum_j exp(s_j - lse) = 1) and its output is the softmax-weighted sum of the
+    context rows under that normaliser, recomputed in fp32 from the same bf16
+    inputs, within the per-row gate of the oracle comparisons."""
+    w = case.w
     cm = relaxkv.CONTEXT_FULL if mode == "full" else relaxkv.CONTEXT_UNION
     R_l = np.asarray(sets_ref.R[l])
     n = len(R_l)
-    fresh = big_case.fresh(l, R_l)
-    out, lse = big_case.gpu_attn(l, fresh, n, cm)
+    fresh = case.fresh(l, R_l)
+    out, lse = case.gpu_attn(l, fresh, n, cm)
     rank = np.full(w.T_c, -1, dtype=np.int64)
     rank[R_l] = np.arange(n)
     if mode == "union":
@@ -315,7 +305,7 @@ def test_full_size_attention_every_target(big_case, mode, l):
     else:
         ctx = np.arange(w.T_c)
         lim = R_l                                  # position of each target's last key
-    K, V = _mixed_context(big_case.kc[l], big_case.vc[l], fresh[1], fresh[2], ctx, rank)
+    K, V = _mixed_context(case.kc[l], case.vc[l], fresh[1], fresh[2], ctx, rank)
     G = w.H // w.H_kv
     scale = 1.0 / math.sqrt(w.d)
     lim_t = torch.as_tensor(lim, device="cuda")
@@ -339,6 +329,35 @@ def test_full_size_attention_every_target(big_case, mode, l):
     assert worst_sum < 5e-3, worst_sum
     assert worst_o < 2e-2, worst_o
     assert worst_rel <= 1.0, worst_rel
+
+
+@pytest.mark.parametrize("mode,l", [("union", 19), ("full", 19), ("union", 39)])
+def test_full_size_attention_every_target(big_case, mode, l):
+    """Every target and head of a 32K layer (|R_l| about 27 500 targets x 40
+    heads at layer 19; the 4 915 targets of the last layer, the sparsest in U,
+    where tiles span the widest staircase and waves skip the most steps): the
+    property check of _every_target_property at full size; the element-wise
+    parity with the oracle is the sampled test above."""
+    a = synthetic_scores(BIG.L, BIG.T_c, seed=5)
+    anchors_ref = oracle.select(a.astype(np.float64), big_case.k)
+    sets_ref = oracle.build_sets(anchors_ref, BIG.T_c)
+    big_case.req.select(torch.from_numpy(a).cuda(), big_case.sets)
+    compare_sets(big_case.gpu_sets(), sets_ref)
+    _every_target_property(big_case, sets_ref, l, mode)
+
+
+@pytest.mark.parametrize("name,ratio,l", [("llama8b-8k", None, 0), ("qwen14b-16k", 0.30, 20)])
+def test_full_size_workload_every_target(gpu_lib, name, ratio, l):
+    """The same property check on every target and head of one layer of the 8K
+    Llama-shaped workload (layer 0: all of U, G = 4) and of the 16K workload at
+    a 30% anchor ratio, on sets from seeded scores."""
+    case = Case(W[name], ratio=ratio)
+    a = synthetic_scores(case.L, case.T, seed=31)
+    anchors_ref = oracle.select(a.astype(np.float64), case.k)
+    sets_ref = oracle.build_sets(anchors_ref, case.T)
+    case.req.select(torch.from_numpy(a).cuda(), case.sets)
+    compare_sets(case.gpu_sets(), sets_ref)
+    _every_target_property(case, sets_ref, l, "union")
 
 
 # ---------------------------------------------------------------- every workload at full size
