@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from harness import Case, assert_close, synthetic_scores
+from harness import assert_close, Case, every_target_property, synthetic_scores
 from paper_2609_33503_amd import relaxkv, synth
 
 pytestmark = pytest.mark.gpu
@@ -131,3 +131,4 @@ def test_full_size_context_variants(gpu_lib, construction):
         ts = sorted(set([0, 1, n // 2, n - 1] + rng.integers(0, n, size=6).tolist()))
         O_ref, lse_ref = case.oracle_attn(l, ref, fresh, targets=ts)
         _compare_attn(case, out[ts], lse[ts], O_ref, lse_ref, f"32K {construction} layer {l}")
+    every_target_property(case, ref, w.L - 1, "union")         # every target of the last layer

@@ -14,7 +14,7 @@ import pytest
 import torch
 
 import oracle
-from harness import Case, assert_close, synthetic_scores
+from harness import assert_close, Case, every_target_property, synthetic_scores
 from paper_2609_33503_amd import relaxkv, synth
 
 pytestmark = pytest.mark.gpu
@@ -233,3 +233,4 @@ def test_full_size_global_target_sweep(gpu_lib):
             ts = sorted(set([0, 1, n_ref // 2, n_ref - 1] + rng.integers(0, n_ref, size=6).tolist()))
             O_ref, lse_ref = case.oracle_attn(l, ref, fresh, targets=ts)
             _compare_attn(case, out[ts], lse[ts], O_ref, lse_ref, f"32K r_g={r} layer {l}")
+        every_target_property(case, ref, w.L - 1, "union")     # every target of the last layer

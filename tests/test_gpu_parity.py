@@ -15,7 +15,7 @@ import pytest
 import torch
 
 import oracle
-from harness import Case, assert_close, compare_sets, synthetic_scores
+from harness import Case, assert_close, compare_sets, every_target_property, synthetic_scores
 from paper_2609_33503_amd import relaxkv, synth
 
 pytestmark = pytest.mark.gpu
@@ -272,78 +272,19 @@ def test_full_size_update_cache_bit_exact(big_case):
     assert torch.equal(v_out[others], big_case.vc[others])
 
 
-def _mixed_context(kc_l, vc_l, fresh_k, fresh_v, ctx, rank):
-    """fp32 K~/V~ [H_kv][|ctx|][d] over the positions ctx: the fresh row of a
-    position with rank >= 0, its cached row otherwise."""
-    idx = torch.as_tensor(ctx, dtype=torch.int64, device=kc_l.device)
-    rk = torch.as_tensor(rank[ctx], dtype=torch.int64, device=kc_l.device)
-    K = kc_l.index_select(1, idx).float()
-    V = vc_l.index_select(1, idx).float()
-    sel = (rk >= 0).nonzero().flatten()
-    K[:, sel] = fresh_k.index_select(0, rk[sel]).float().transpose(0, 1)
-    V[:, sel] = fresh_v.index_select(0, rk[sel]).float().transpose(0, 1)
-    return K.contiguous(), V.contiguous()
-
-
-def _every_target_property(case, sets_ref, l, mode):
-    """Every target and head of layer l in the benchmark's launch configuration:
-    the kernel's log-sum-exp normalises the softmax of its own context
-    (sum_j exp(s_j - lse) = 1) and its output is the softmax-weighted sum of the
-    context rows under that normaliser, recomputed in fp32 from the same bf16
-    inputs, within the per-row gate of the oracle comparisons."""
-    w = case.w
-    cm = relaxkv.CONTEXT_FULL if mode == "full" else relaxkv.CONTEXT_UNION
-    R_l = np.asarray(sets_ref.R[l])
-    n = len(R_l)
-    fresh = case.fresh(l, R_l)
-    out, lse = case.gpu_attn(l, fresh, n, cm)
-    rank = np.full(w.T_c, -1, dtype=np.int64)
-    rank[R_l] = np.arange(n)
-    if mode == "union":
-        ctx = np.asarray(sets_ref.U)
-        lim = np.asarray(sets_ref.R_u[l])          # compact index of each target's last key
-    else:
-        ctx = np.arange(w.T_c)
-        lim = R_l                                  # position of each target's last key
-    K, V = _mixed_context(case.kc[l], case.vc[l], fresh[1], fresh[2], ctx, rank)
-    G = w.H // w.H_kv
-    scale = 1.0 / math.sqrt(w.d)
-    lim_t = torch.as_tensor(lim, device="cuda")
-    keys = torch.arange(len(ctx), device="cuda")
-    worst_sum, worst_o, worst_rel = 0.0, 0.0, 0.0
-    for t0 in range(0, n, 256):
-        t1 = min(n, t0 + 256)
-        mask = keys[None, :] > lim_t[t0:t1, None]                              # [c][|ctx|]
-        for g in range(w.H_kv):
-            q = fresh[0][t0:t1, g * G:(g + 1) * G].float().reshape(-1, w.d)    # [c*G][d]
-            s = torch.matmul(q, K[g].t()) * scale                             # [c*G][|ctx|]
-            s = s.view(t1 - t0, G, -1).masked_fill(mask[:, None, :], -math.inf)
-            p = torch.exp(s - lse[t0:t1, g * G:(g + 1) * G, None])
-            worst_sum = max(worst_sum, float((p.sum(-1) - 1.0).abs().max()))
-            o_ref = torch.matmul(p.view(-1, len(ctx)), V[g]).view(t1 - t0, G, w.d)
-            o = out[t0:t1, g * G:(g + 1) * G].float()
-            err = (o - o_ref).abs().amax(-1)
-            worst_o = max(worst_o, float(err.max()))
-            # the per-row gate of the oracle comparisons: 1e-2 of the row's largest |O| + 1e-6
-            worst_rel = max(worst_rel, float((err / (1e-2 * o_ref.abs().amax(-1) + 1e-6)).max()))
-    assert worst_sum < 5e-3, worst_sum
-    assert worst_o < 2e-2, worst_o
-    assert worst_rel <= 1.0, worst_rel
-
-
 @pytest.mark.parametrize("mode,l", [("union", 19), ("full", 19), ("union", 39)])
 def test_full_size_attention_every_target(big_case, mode, l):
     """Every target and head of a 32K layer (|R_l| about 27 500 targets x 40
     heads at layer 19; the 4 915 targets of the last layer, the sparsest in U,
     where tiles span the widest staircase and waves skip the most steps): the
-    property check of _every_target_property at full size; the element-wise
+    property check of harness.every_target_property at full size; the element-wise
     parity with the oracle is the sampled test above."""
     a = synthetic_scores(BIG.L, BIG.T_c, seed=5)
     anchors_ref = oracle.select(a.astype(np.float64), big_case.k)
     sets_ref = oracle.build_sets(anchors_ref, BIG.T_c)
     big_case.req.select(torch.from_numpy(a).cuda(), big_case.sets)
     compare_sets(big_case.gpu_sets(), sets_ref)
-    _every_target_property(big_case, sets_ref, l, mode)
+    every_target_property(big_case, sets_ref, l, mode)
 
 
 @pytest.mark.parametrize("name,ratio,l", [("llama8b-8k", None, 0), ("qwen14b-16k", 0.30, 20)])
@@ -357,7 +298,7 @@ def test_full_size_workload_every_target(gpu_lib, name, ratio, l):
     sets_ref = oracle.build_sets(anchors_ref, case.T)
     case.req.select(torch.from_numpy(a).cuda(), case.sets)
     compare_sets(case.gpu_sets(), sets_ref)
-    _every_target_property(case, sets_ref, l, "union")
+    every_target_property(case, sets_ref, l, "union")
 
 
 # ---------------------------------------------------------------- every workload at full size
