@@ -246,7 +246,8 @@ __global__ __launch_bounds__((NB + NH) * 64) void qattn_bf16(QaArgs a) {
         const float mx = qa_pair_max(NKB == 2 ? fmaxf(mk[0], mk[NKB - 1]) : mk[0]) * a.sl2;
         if (__any(mx > m_run + kQaSlack)) {
             const float m_new = mx > m_run + kQaSlack ? mx : m_run;
-            const float alpha = fast_exp2(m_run - m_new);
+            // (a row whose max stays -inf keeps its zero sum and output)
+            const float alpha = m_new == m_run ? 1.f : fast_exp2(m_run - m_new);
             l_run *= alpha;
 #pragma unroll
             for (int db = 0; db < DB; ++db) o[db] *= alpha;
@@ -254,12 +255,18 @@ __global__ __launch_bounds__((NB + NH) * 64) void qattn_bf16(QaArgs a) {
         }
         // The row sum adds the bf16 probabilities that the PV product uses, two
         // per dot2 instruction, in four chains.
+        // A key-half wave can meet tiles whose keys are all masked before its
+        // first visible key (the last split's cache tail when it holds at most
+        // 32 keys, the causal query tiles): its running max is still -inf
+        // there, and exp2 of -inf - (-inf) would be NaN.  Those tiles use a
+        // reference of 0 instead, so they add exact zeros.
+        const float m_ref = m_run == -INFINITY ? 0.f : m_run;
         bf16x8 pb[NKB][2];
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
-                pb[kb][v >> 3][v & 7] = (__bf16)fast_exp2(fmaf(s[kb][v], a.sl2, -m_run));
+                pb[kb][v >> 3][v & 7] = (__bf16)fast_exp2(fmaf(s[kb][v], a.sl2, -m_ref));
         {
             typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
             const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};

@@ -433,7 +433,10 @@ __global__ __launch_bounds__(256) void score_colsum_f32(const float* __restrict_
     const int i = blockIdx.x * 256 + threadIdx.x;
     const int l = blockIdx.y;
     if (i >= T) return;
-    float acc = 0.f;
+    // Summed in double: a key's column takes H * Qn terms (thousands for long
+    // queries and wide GQA groups), and a float running sum of that many terms
+    // drifts by more than the 1e-5 the fp32 path has to meet after MinMax.
+    double acc = 0.0;
     for (int g = 0; g < Hkv; ++g) {
         float kr[D];
         const float* kp = kc + (((size_t)l * Hkv + g) * T + i) * D;
@@ -448,11 +451,11 @@ __global__ __launch_bounds__(256) void score_colsum_f32(const float* __restrict_
                 for (int e = 0; e < D; ++e) s = fmaf(qr[e], kr[e], s);
                 const float lse = q_lse ? q_lse[((size_t)l * Qn + t) * H + h]
                                         : lse_nat[((size_t)l * Hkv + g) * rows_pad + t * G + hh];
-                acc += expf(s * scale - lse);
+                acc += (double)expf(s * scale - lse);
             }
         }
     }
-    part[(size_t)l * T + i] = acc;
+    part[(size_t)l * T + i] = (float)acc;
 }
 
 // ---------------------------------------------------------------- finaliser

@@ -29,6 +29,9 @@ SMALL = {
     "rows288": synth.shrink(W["llama8b-8k"], L=2, T_c=1100, Qn=72),
     "rows320-d64": synth.shrink(W["qwen14b-16k"], L=2, T_c=1000, d=64),
     "fp32-d128": synth.shrink(W["tiny-2L-1k-fp32"], L=2, T_c=300, d=128, H=6, H_kv=3, Qn=5),
+    # 320 rows (key-half waves) with a last split of 16 cache keys and 64 query tokens:
+    # the key-half waves meet fully masked tiles before their first visible key
+    "half-tail": synth.shrink(W["qwen14b-16k"], L=1, T_c=1040),
     # 32 key splits (the merge kernel for exactly 32) and 34 (the general merge)
     "splits32": synth.shrink(W["llama8b-8k"], L=1, T_c=8192, Qn=8),
     "many-splits": synth.shrink(W["llama8b-8k"], L=1, T_c=8500, H=4, H_kv=2, Qn=8),

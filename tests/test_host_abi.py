@@ -94,6 +94,7 @@ def test_validate(rk, kw, status):
     (dict(T_c=32768, H=40, H_kv=8, n_query=64), 32),
     (dict(T_c=8500, H=4, H_kv=2, n_query=8), 34),
     (dict(T_c=8192, H=32, H_kv=8, n_query=8), 32),
+    (dict(T_c=1040, H=40, H_kv=8, n_query=64), 5),     # the last split holds 16 keys
     (dict(T_c=1500, H=32, H_kv=8, n_query=64), 6),
 ])
 def test_query_workspace_split_count(rk, kw, n_split):
