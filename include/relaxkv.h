@@ -118,6 +118,19 @@ typedef int32_t relaxkv_status;
  *              the scoring softmax runs over the T_c cached keys only and
  *              relaxkv_score computes the normaliser itself (two passes over K);
  *              when given, relaxkv_score reads K once.
+ *   kv_stride_layer, kv_stride_head, kv_stride_token
+ *              element strides of k_cache and v_cache (both laid out alike, and
+ *              so are the cache arguments of relaxkv_update_cache and
+ *              relaxkv_query_attn): the d contiguous elements of token i of KV
+ *              head g of layer l start at element l * kv_stride_layer +
+ *              g * kv_stride_head + i * kv_stride_token.  0 selects the dense
+ *              value (d, T_c * token stride, H_kv * head stride), so a zeroed
+ *              descriptor describes [L][H_kv][T_c][d]; a cache allocated for
+ *              more tokens than T_c, or laid out [L][T_c][H_kv][d], is passed
+ *              with its own strides.  Every other array (q, q_lse, the fresh
+ *              rows, the outputs) is dense row-major.
+ * Pointers: q, k_cache and v_cache 16-byte aligned, and every cache row too
+ * (strides times the element size a multiple of 16 bytes).
  */
 typedef struct relaxkv_problem {
     int32_t L, T_c, n_query, H, H_kv, d;
@@ -128,6 +141,7 @@ typedef struct relaxkv_problem {
     const void* k_cache;
     const void* v_cache;
     const float* q_lse;
+    int64_t kv_stride_layer, kv_stride_head, kv_stride_token;
 } relaxkv_problem;
 
 /*
@@ -199,10 +213,16 @@ const char* relaxkv_status_string(relaxkv_status s);
  * r is not a finite number in [0, 1] or T_c < 1. */
 int32_t relaxkv_anchor_count(double anchor_ratio, int32_t T_c);
 
-/* Host only.  Checks dimensions, pointers, dtype and the ratio of `p`:
- * RELAXKV_EINVAL for a bad dimension, pointer, scale or ratio,
+/* Host only.  Checks dimensions, pointers, dtype, strides and the ratio of `p`:
+ * RELAXKV_EINVAL for a bad dimension, pointer, scale or ratio, a negative
+ * stride, or cache strides that do not nest: taken from the smallest, the
+ * stride of each dimension with more than one entry must step past the whole
+ * extent of the dimensions inside it, so that no two rows overlap (dimensions
+ * of size 1 are ignored),
  * RELAXKV_EUNSUPPORTED for a head_dim, dtype, GQA group or bf16 layer size
- * (see the limits above) this build has no kernel for. */
+ * (see the limits above) this build has no kernel for, a pointer or cache row
+ * that is not 16-byte aligned, or (bf16) a token stride of 2^24 elements or
+ * more or with (T_c - 1) * stride + d >= RELAXKV_MAX_BF16_LAYER_ELEMS. */
 relaxkv_status relaxkv_validate(const relaxkv_problem* p);
 
 /* Host only.  Device scratch bytes relaxkv_score needs (0 when p is invalid). */

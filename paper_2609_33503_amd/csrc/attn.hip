@@ -46,7 +46,7 @@ struct AttnArgs {
     const void* q_new;
     const void* k_new;
     const void* v_new;
-    const void* kc;          // layer base [H_kv][T][d]
+    const void* kc;          // layer base: row i of KV head g at element g * kv_sh + i * kv_st
     const void* vc;
     const int32_t* U;
     const int32_t* cidx;
@@ -60,6 +60,7 @@ struct AttnArgs {
     uint32_t* tiles;         // this layer's and mode's work counters: [Hkv] next tile, [Hkv] workgroups
     void* out;
     float* lse;
+    int64_t kv_sh, kv_st;    // element strides of the cache's KV heads and tokens
     int H, Hkv, G, T, layer;
     int cap;                 // rows this launch may process (row capacity, host bound)
     float scale;             // softmax scale (natural units)
@@ -67,7 +68,7 @@ struct AttnArgs {
 
 // Row of key index c for KV head g: returns the element offset of that row in
 // either the fresh tensor (fresh = true) or the cached layer.
-template <bool FULL>
+template <int D, bool FULL>
 __device__ __forceinline__ size_t kv_row(const AttnArgs& a, int c, int g, bool& fresh) {
     int pos, r;
     if (FULL) {
@@ -78,7 +79,7 @@ __device__ __forceinline__ size_t kv_row(const AttnArgs& a, int c, int g, bool& 
         r = a.src_l[c];
     }
     fresh = r >= 0;
-    return fresh ? ((size_t)r * a.Hkv + g) : ((size_t)g * a.T + pos);
+    return fresh ? ((size_t)r * a.Hkv + g) * D : (size_t)(g * a.kv_sh + pos * a.kv_st);
 }
 
 // ----------------------------------------------------------------- bf16 MFMA
@@ -204,8 +205,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     // Row bases of the fresh rows (stride Hkv*D) and of the cached layer (stride D).
     const uint16_t* kng = (const uint16_t*)a.k_new + (size_t)g * D;
     const uint16_t* vng = (const uint16_t*)a.v_new + (size_t)g * D;
-    const uint16_t* kcg = (const uint16_t*)a.kc + (size_t)g * a.T * D;
-    const uint16_t* vcg = (const uint16_t*)a.vc + (size_t)g * a.T * D;
+    const uint16_t* kcg = (const uint16_t*)a.kc + g * a.kv_sh;
+    const uint16_t* vcg = (const uint16_t*)a.vc + g * a.kv_sh;
+    const uint32_t kst = (uint32_t)a.kv_st;              // < 2^24 (checked on the host)
     const int32_t* srcmap = FULL ? a.rank_l : a.src_l;
     const int S = cmax / TK + 1;                     // 64-key steps
 
@@ -243,9 +245,10 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
                 // (the empty asm statements keep the compiler from turning the
                 // fresh/cached choice into a divergent branch)
                 const bool fresh = r >= 0;
-                // element offset of the row's chunk (< 2^31: T_c * D and |R_l| * Hkv * D)
-                const uint32_t off = (fresh ? (uint32_t)r * (uint32_t)(Hkv * D)
-                                            : (uint32_t)pos * (uint32_t)D) + choff;
+                // element offset of the row's chunk (< 2^31: (T_c - 1) * kst + D and
+                // |R_l| * Hkv * D, both checked on the host, so 24-bit multiplies do)
+                const uint32_t off = (fresh ? __umul24((uint32_t)r, (uint32_t)(Hkv * D))
+                                            : __umul24((uint32_t)pos, kst)) + choff;
                 const uint64_t kb = fresh ? (uint64_t)kng : (uint64_t)kcg;
                 const uint64_t vb = fresh ? (uint64_t)vng : (uint64_t)vcg;
                 const uint16_t* kp = (const uint16_t*)kb + off;
@@ -427,7 +430,10 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
     if (!valid) return;
     const bool empty = lim < 0;
     const float inv = empty ? 0.f : 1.0f / l_tot;
-    uint16_t* out = (uint16_t*)a.out + ((size_t)t_row * a.H + head) * D;
+    // (t, head) row index: below T_c * H <= 2^32, and one register where a 64-bit
+    // product held across the loop would take two
+    const uint32_t orow = (uint32_t)t_row * (uint32_t)a.H + (uint32_t)head;
+    uint16_t* out = (uint16_t*)a.out + (size_t)orow * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -441,7 +447,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16(AttnArgs a) {
         }
     }
     if (a.lse && hf == 0)
-        a.lse[(size_t)t_row * a.H + head] = empty ? -INFINITY : (m_run + __log2f(l_tot)) * kLn2;
+        a.lse[orow] = empty ? -INFINITY : (m_run + __log2f(l_tot)) * kLn2;
 }
 
 
@@ -483,9 +489,9 @@ __global__ __launch_bounds__(64) void attn_f32(AttnArgs a) {
         const float* vrow = nullptr;
         if (c <= lim) {
             bool fresh;
-            const size_t row = kv_row<FULL>(a, c, g, fresh);
-            const float* kr = (fresh ? kn : kc) + row * D;
-            vrow = (fresh ? vn : vc) + row * D;
+            const size_t row = kv_row<D, FULL>(a, c, g, fresh);
+            const float* kr = (fresh ? kn : kc) + row;
+            vrow = (fresh ? vn : vc) + row;
             float acc = 0.f;
             for (int e = 0; e < D; ++e) acc = fmaf(qs[e], kr[e], acc);
             s = acc * a.scale;
@@ -537,13 +543,15 @@ hipError_t launch_sparse_attn(const relaxkv_problem& p, const relaxkv_sets& s, i
                               hipStream_t st) {
     const bool bf16 = p.dtype == RELAXKV_DTYPE_BF16;
     const size_t esz = bf16 ? 2 : 4;
-    const size_t layer_elems = (size_t)p.H_kv * p.T_c * p.d;
+    const KvStrides ks = kv_strides(p);
     AttnArgs a;
     a.q_new = q_new;
     a.k_new = k_new;
     a.v_new = v_new;
-    a.kc = (const char*)p.k_cache + (size_t)layer * layer_elems * esz;
-    a.vc = (const char*)p.v_cache + (size_t)layer * layer_elems * esz;
+    a.kc = (const char*)p.k_cache + (size_t)(layer * ks.layer) * esz;
+    a.vc = (const char*)p.v_cache + (size_t)(layer * ks.layer) * esz;
+    a.kv_sh = ks.head;
+    a.kv_st = ks.token;
     // The layer's context list: the union, or a construction variant's list.
     a.U = s.context_sets == RELAXKV_CONTEXT_SETS_GLOBAL      ? s.ctx
           : s.context_sets == RELAXKV_CONTEXT_SETS_LAYERWISE ? s.ctx + (size_t)layer * p.T_c

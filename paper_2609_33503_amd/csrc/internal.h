@@ -9,6 +9,20 @@
 
 namespace relaxkv {
 
+// Element strides of k_cache and v_cache (layer, KV head, token), the
+// descriptor's zeros replaced by the dense values.
+struct KvStrides {
+    int64_t layer, head, token;
+};
+
+inline KvStrides kv_strides(const relaxkv_problem& p) {
+    KvStrides s;
+    s.token = p.kv_stride_token ? p.kv_stride_token : p.d;
+    s.head = p.kv_stride_head ? p.kv_stride_head : (int64_t)p.T_c * s.token;
+    s.layer = p.kv_stride_layer ? p.kv_stride_layer : (int64_t)p.H_kv * s.head;
+    return s;
+}
+
 // Scratch layout of relaxkv_score (offsets in bytes from the workspace base).
 struct ScoreWorkspace {
     size_t part_off;    // float [L][n_part][T_c]   per-KV-head pooled partial sums

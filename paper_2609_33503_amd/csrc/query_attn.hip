@@ -54,12 +54,13 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 struct QaArgs {
     const uint16_t* q;       // this layer's query rows [Qn][H][D]
-    const uint16_t* kc;      // this layer's cache [Hkv][T][D]
+    const uint16_t* kc;      // this layer's cache: row i of KV head g at element g * kv_sh + i * kv_st
     const uint16_t* vc;
     const uint16_t* kq;      // the query tokens' keys/values [Qn][Hkv][D]
     const uint16_t* vq;
     uint16_t* part_o;        // [n_split][Hkv][rows_pad][D] bf16 normalised partial outputs
     float* part_l;           // [n_split][Hkv][rows_pad] log2-sum-exp of each partial
+    int64_t kv_sh, kv_st;    // element strides of the cache's KV heads and tokens
     int T, Qn, H, Hkv, G, n_rows, rows_pad, n_split, kps;   // kps: cache keys per split
     float sl2;               // softmax scale * log2(e)
 };
@@ -152,7 +153,7 @@ __global__ __launch_bounds__((NB + NH) * 64) void qattn_bf16(QaArgs a) {
                 const int row = jj * RPI + lr;
                 const int kk = min(k0 + row, kmax);
                 const size_t e = qt ? ((size_t)kk * a.Hkv + g) * D
-                                    : ((size_t)g * a.T + key0 + kk) * D;
+                                    : (size_t)(g * a.kv_sh + (key0 + kk) * a.kv_st);
                 const uint16_t* base = qt ? (isv ? a.vq : a.kq) : (isv ? a.vc : a.kc);
                 uint16_t* dst = (isv ? Vt[st] : Kt[st]) + jj * RPI * D;
                 load_lds16(base + e + ((pc ^ tile_swz<D>(row)) << 3), dst);
@@ -168,7 +169,7 @@ __global__ __launch_bounds__((NB + NH) * 64) void qattn_bf16(QaArgs a) {
         const bool isv = j >= NL;
         const int jj = isv ? j - NL : j;
         const int row = jj * RPI + lrow;
-        cbase[i] = (isv ? a.vc : a.kc) + ((size_t)g * a.T + key0 + row) * D +
+        cbase[i] = (isv ? a.vc : a.kc) + g * a.kv_sh + (key0 + row) * a.kv_st +
                    ((pchunk ^ tile_swz<D>(row)) << 3);
     }
     auto issue_full = [&](int tt) {
@@ -180,7 +181,7 @@ __global__ __launch_bounds__((NB + NH) * 64) void qattn_bf16(QaArgs a) {
                 const bool isv = j >= NL;
                 const int jj = isv ? j - NL : j;
                 uint16_t* dst = (isv ? Vt[st] : Kt[st]) + jj * RPI * D;
-                load_lds16(cbase[i] + (size_t)tt * TK * D, dst);
+                load_lds16(cbase[i] + tt * TK * a.kv_st, dst);
             }
         }
     };
@@ -483,8 +484,8 @@ __global__ __launch_bounds__(64) void qattn_f32(const float* __restrict__ q,
                                                 const float* __restrict__ kc,
                                                 const float* __restrict__ vc,
                                                 const float* __restrict__ kq,
-                                                const float* __restrict__ vq, int T, int H,
-                                                int Hkv, int G, float scale,
+                                                const float* __restrict__ vq, KvStrides ks,
+                                                int T, int H, int Hkv, int G, float scale,
                                                 float* __restrict__ out, float* __restrict__ lse) {
     constexpr int DPL = D / 64;
     __shared__ float qs[D];
@@ -502,8 +503,9 @@ __global__ __launch_bounds__(64) void qattn_f32(const float* __restrict__ q,
         float s = -INFINITY;
         const float* vrow = nullptr;
         if (c < nk) {
-            const float* krow = c < T ? kc + ((size_t)g * T + c) * D : kq + ((size_t)(c - T) * Hkv + g) * D;
-            vrow = c < T ? vc + ((size_t)g * T + c) * D : vq + ((size_t)(c - T) * Hkv + g) * D;
+            const int64_t ce = g * ks.head + c * ks.token;          // cache row element offset
+            const float* krow = c < T ? kc + ce : kq + ((size_t)(c - T) * Hkv + g) * D;
+            vrow = c < T ? vc + ce : vq + ((size_t)(c - T) * Hkv + g) * D;
             float acc = 0.f;
             for (int e = 0; e < D; ++e) acc = fmaf(qs[e], krow[e], acc);
             s = acc * scale;
@@ -582,27 +584,30 @@ hipError_t launch_query_attn(const relaxkv_problem& p, int layer, const void* k_
                              float* lse_out, char* ws, hipStream_t st) {
     const int G = p.H / p.H_kv;
     const float scale = p.softmax_scale > 0.f ? p.softmax_scale : 1.0f / sqrtf((float)p.d);
-    const size_t cache_layer = (size_t)p.H_kv * p.T_c * p.d;
+    const KvStrides ks = kv_strides(p);
+    const size_t cache_layer = (size_t)(layer * ks.layer);     // this layer's first element
     const size_t q_layer = (size_t)p.n_query * p.H * p.d;
     if (p.dtype == RELAXKV_DTYPE_F32) {
         const float* q = (const float*)p.q + (size_t)layer * q_layer;
-        const float* kc = (const float*)k_cache + (size_t)layer * cache_layer;
-        const float* vc = (const float*)v_cache + (size_t)layer * cache_layer;
+        const float* kc = (const float*)k_cache + cache_layer;
+        const float* vc = (const float*)v_cache + cache_layer;
         if (p.d == 128)
             hipLaunchKernelGGL(qattn_f32<128>, dim3(p.n_query, p.H), dim3(64), 0, st, q, kc, vc,
-                               (const float*)k_q, (const float*)v_q, p.T_c, p.H, p.H_kv, G, scale,
+                               (const float*)k_q, (const float*)v_q, ks, p.T_c, p.H, p.H_kv, G, scale,
                                (float*)out, lse_out);
         else
             hipLaunchKernelGGL(qattn_f32<64>, dim3(p.n_query, p.H), dim3(64), 0, st, q, kc, vc,
-                               (const float*)k_q, (const float*)v_q, p.T_c, p.H, p.H_kv, G, scale,
+                               (const float*)k_q, (const float*)v_q, ks, p.T_c, p.H, p.H_kv, G, scale,
                                (float*)out, lse_out);
         return hipGetLastError();
     }
     const QueryAttnWorkspace w = query_attn_workspace_layout(p);
     QaArgs a;
     a.q = (const uint16_t*)p.q + (size_t)layer * q_layer;
-    a.kc = (const uint16_t*)k_cache + (size_t)layer * cache_layer;
-    a.vc = (const uint16_t*)v_cache + (size_t)layer * cache_layer;
+    a.kc = (const uint16_t*)k_cache + cache_layer;
+    a.vc = (const uint16_t*)v_cache + cache_layer;
+    a.kv_sh = ks.head;
+    a.kv_st = ks.token;
     a.kq = (const uint16_t*)k_q;
     a.vq = (const uint16_t*)v_q;
     a.part_o = (uint16_t*)(ws + w.part_o_off);

@@ -58,6 +58,44 @@ bool sets_match(const relaxkv_problem* p, const relaxkv_sets* s) {
            s->context_sets <= RELAXKV_CONTEXT_SETS_LAYERWISE;
 }
 
+// The cache strides: none negative; no two rows overlap, i.e. taken from the
+// smallest, each stride of a dimension with more than one entry steps past the
+// whole extent of the dimensions inside it; 16-byte aligned rows and pointers
+// (the kernels move rows in 16-byte pieces); and, for bf16, cached-row offsets
+// within a head that fit the attention's 32-bit element offsets.
+relaxkv_status strides_status(const relaxkv_problem* p) {
+    if (p->kv_stride_layer < 0 || p->kv_stride_head < 0 || p->kv_stride_token < 0)
+        return RELAXKV_EINVAL;
+    const KvStrides s = kv_strides(*p);
+    struct Dim { int64_t stride, n; } dims[3] = {{s.token, p->T_c}, {s.head, p->H_kv},
+                                                  {s.layer, p->L}};
+    for (int i = 1; i < 3; ++i)                          // ascending strides (insertion sort)
+        for (int j = i; j > 0 && dims[j].stride < dims[j - 1].stride; --j) {
+            const Dim t = dims[j];
+            dims[j] = dims[j - 1];
+            dims[j - 1] = t;
+        }
+    int64_t extent = p->d;                               // elements spanned by the inner dimensions
+    for (const Dim& dm : dims) {
+        if (dm.n <= 1) continue;
+        if (dm.stride < extent) return RELAXKV_EINVAL;
+        // (n - 1) * stride + extent, guarded against int64 overflow
+        if (dm.stride > (INT64_MAX - extent) / (dm.n - 1)) return RELAXKV_EINVAL;
+        extent += (dm.n - 1) * dm.stride;
+    }
+    const int64_t esz = p->dtype == RELAXKV_DTYPE_BF16 ? 2 : 4;
+    if ((s.layer * esz) % 16 || (s.head * esz) % 16 || (s.token * esz) % 16)
+        return RELAXKV_EUNSUPPORTED;
+    if ((uintptr_t)p->q % 16 || (uintptr_t)p->k_cache % 16 || (uintptr_t)p->v_cache % 16)
+        return RELAXKV_EUNSUPPORTED;
+    // (the bf16 attention forms the offset with a 24-bit multiply)
+    if (p->dtype == RELAXKV_DTYPE_BF16 &&
+        (s.token >= ((int64_t)1 << 24) ||
+         (int64_t)(p->T_c - 1) * s.token + p->d >= RELAXKV_MAX_BF16_LAYER_ELEMS))
+        return RELAXKV_EUNSUPPORTED;
+    return RELAXKV_OK;
+}
+
 relaxkv_status from_hip(hipError_t e) { return e == hipSuccess ? RELAXKV_OK : RELAXKV_EDEVICE; }
 
 }  // namespace
@@ -101,7 +139,7 @@ relaxkv_status relaxkv_validate(const relaxkv_problem* p) {
     if (p->dtype == RELAXKV_DTYPE_BF16 &&
         (int64_t)p->T_c * p->H_kv * p->d >= RELAXKV_MAX_BF16_LAYER_ELEMS)
         return RELAXKV_EUNSUPPORTED;
-    return RELAXKV_OK;
+    return strides_status(p);
 }
 
 size_t relaxkv_score_workspace_bytes(const relaxkv_problem* p) {

@@ -107,11 +107,11 @@ __device__ __forceinline__ void stage_lse(float (*Ls)[2][16], int nt, int l, int
 // past T re-read key T-1 (their results are masked or never stored).
 template <int D, int NKB>
 __device__ __forceinline__ void load_keys(bf16x8 (&dst)[NKB][D / 16], const uint16_t* Kg, int T,
-                                          int kr, int r32, int hf) {
+                                          int64_t sT, int kr, int r32, int hf) {
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
         const int key = min(kr + 32 * kb + r32, T - 1);
-        const bf16x8* kp = (const bf16x8*)(Kg + (size_t)key * D + hf * 8);
+        const bf16x8* kp = (const bf16x8*)(Kg + key * sT + hf * 8);
 #pragma unroll
         for (int j = 0; j < D / 16; ++j) dst[kb][j] = kp[2 * j];
     }
@@ -136,7 +136,7 @@ __device__ __forceinline__ void load_keys(bf16x8 (&dst)[NKB][D / 16], const uint
 // another inside a row chunk.
 template <int D, int NW, int NKB>
 __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, KvStrides ks, int T, int Qn, int H,
     int Hkv, int G, int n_rows, int rows_pad, int keys_per_split, float sl2,
     const float* __restrict__ lse2, const float* __restrict__ q_lse, float* __restrict__ part) {
     constexpr int KS = D / 16;                      // k-steps of the dot product
@@ -149,13 +149,13 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
     const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, hf = lane >> 5;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
+    const uint16_t* Kg = kc + l * ks.layer + g * ks.head;
     float* part_g = part + ((size_t)l * Hkv + g) * T;
     const int key0 = split * keys_per_split;
     const int key1 = min(T, key0 + keys_per_split);
 
     bf16x8 kf[NKB][KS];
-    auto load_k = [&](bf16x8 (&dst)[NKB][KS], int kr) { load_keys<D, NKB>(dst, Kg, T, kr, r32, hf); };
+    auto load_k = [&](bf16x8 (&dst)[NKB][KS], int kr) { load_keys<D, NKB>(dst, Kg, T, ks.token, kr, r32, hf); };
 
     for (int rc0 = 0; rc0 < rows_pad; rc0 += NRB * 32) {
         const int nrb = min(NRB, (rows_pad - rc0) / 32);
@@ -219,7 +219,7 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kreg(
 // into stats[l][g][split][row].
 template <int D, int NW, int NKB>
 __global__ __launch_bounds__(NW * 64) void score_stats_kreg(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, int T, int Qn, int H,
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, KvStrides ks, int T, int Qn, int H,
     int Hkv, int G, int n_rows, int rows_pad, int keys_per_split, int n_split, float sl2,
     float2* __restrict__ stats) {
     constexpr int KS = D / 16;
@@ -232,7 +232,7 @@ __global__ __launch_bounds__(NW * 64) void score_stats_kreg(
     const int split = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, r32 = lane & 31, hf = lane >> 5;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint16_t* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
+    const uint16_t* Kg = kc + l * ks.layer + g * ks.head;
     const int key0 = split * keys_per_split;
     const int key1 = min(T, key0 + keys_per_split);
     bf16x8 kf[NKB][KS];
@@ -252,7 +252,7 @@ __global__ __launch_bounds__(NW * 64) void score_stats_kreg(
             moved[rb] = false;
         }
         int kr = key0 + w * KPW;
-        if (kr < key1) load_keys<D, NKB>(kf, Kg, T, kr, r32, hf);
+        if (kr < key1) load_keys<D, NKB>(kf, Kg, T, ks.token, kr, r32, hf);
         for (; kr < key1; kr += KPR) {
 #pragma unroll
             for (int rb = 0; rb < NRB; ++rb) {
@@ -268,7 +268,7 @@ __global__ __launch_bounds__(NW * 64) void score_stats_kreg(
                                 kf[kb][j], qj, j == 0 ? f32x16{} : acc[kb], 0, 0, 0);
                     }
                     if (rb == nrb - 1 && kr + KPR < key1)
-                        load_keys<D, NKB>(kf, Kg, T, kr + KPR, r32, hf);
+                        load_keys<D, NKB>(kf, Kg, T, ks.token, kr + KPR, r32, hf);
 #pragma unroll
                     for (int kb = 0; kb < NKB; ++kb) {
                         // acc[kb][v] is key kr + 32 kb + 8(v/4) + 4 hf + v%4 of the row.
@@ -374,7 +374,7 @@ __global__ void score_merge(const float2* __restrict__ stats, int n_groups, int 
 
 template <int D>
 __global__ __launch_bounds__(256) void score_stats_f32(const float* __restrict__ q,
-                                                       const float* __restrict__ kc, int T,
+                                                       const float* __restrict__ kc, KvStrides ks, int T,
                                                        int Qn, int H, int Hkv, int G,
                                                        int rows_pad, float scale,
                                                        float* __restrict__ lse_nat) {
@@ -386,10 +386,10 @@ __global__ __launch_bounds__(256) void score_stats_f32(const float* __restrict__
     const int tid = threadIdx.x;
     for (int e = tid; e < D; e += 256) qs[e] = q[((size_t)l * Qn + t) * H * D + (size_t)h * D + e];
     __syncthreads();
-    const float* Kg = kc + ((size_t)l * Hkv + g) * (size_t)T * D;
+    const float* Kg = kc + l * ks.layer + g * ks.head;
     float m = -INFINITY, z = 0.f;
     for (int i = tid; i < T; i += 256) {
-        const float* kr = Kg + (size_t)i * D;
+        const float* kr = Kg + i * ks.token;
         float s = 0.f;
         for (int e = 0; e < D; ++e) s = fmaf(qs[e], kr[e], s);
         s *= scale;
@@ -424,7 +424,7 @@ __global__ __launch_bounds__(256) void score_stats_f32(const float* __restrict__
 
 template <int D>
 __global__ __launch_bounds__(256) void score_colsum_f32(const float* __restrict__ q,
-                                                        const float* __restrict__ kc, int T,
+                                                        const float* __restrict__ kc, KvStrides ks, int T,
                                                         int Qn, int H, int Hkv, int G,
                                                         int rows_pad, float scale,
                                                         const float* __restrict__ lse_nat,
@@ -439,7 +439,7 @@ __global__ __launch_bounds__(256) void score_colsum_f32(const float* __restrict_
     double acc = 0.0;
     for (int g = 0; g < Hkv; ++g) {
         float kr[D];
-        const float* kp = kc + (((size_t)l * Hkv + g) * T + i) * D;
+        const float* kp = kc + l * ks.layer + g * ks.head + i * ks.token;
 #pragma unroll
         for (int e = 0; e < D; ++e) kr[e] = kp[e];
         for (int hh = 0; hh < G; ++hh) {
@@ -557,14 +557,14 @@ void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char*
     const dim3 kgrid((p.T_c + kps - 1) / kps, p.H_kv, p.L);
     if (!p.q_lse) {
         hipLaunchKernelGGL((score_stats_kreg<D, KNW, KNKB>), kgrid, dim3(KNW * 64), 0, st, q, kc,
-                           p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, kps, w.n_split,
+                           kv_strides(p), p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, kps, w.n_split,
                            sl2, stats);
         const long n = (long)p.L * p.H_kv * w.rows_pad;
         hipLaunchKernelGGL(score_merge, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                            (const float2*)stats, p.L * p.H_kv, w.n_split, w.rows_pad, n_rows, lse2);
     }
     hipLaunchKernelGGL((score_colsum_kreg<D, KNW, KNKB>), kgrid, dim3(KNW * 64), 0, st, q, kc,
-                       p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, kps, sl2,
+                       kv_strides(p), p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, kps, sl2,
                        (const float*)lse2, p.q_lse, part);
 }
 
@@ -586,9 +586,9 @@ hipError_t launch_score_f32(const relaxkv_problem& p, const ScoreWorkspace& w, c
     float* lse = (float*)(ws + w.lse_off);
     if (!p.q_lse)
         hipLaunchKernelGGL(score_stats_f32<D>, dim3(p.n_query * p.H, p.L), dim3(256), 0, st, q, kc,
-                           p.T_c, p.n_query, p.H, p.H_kv, G, w.rows_pad, scale, lse);
+                           kv_strides(p), p.T_c, p.n_query, p.H, p.H_kv, G, w.rows_pad, scale, lse);
     hipLaunchKernelGGL(score_colsum_f32<D>, dim3((p.T_c + 255) / 256, p.L), dim3(256), 0, st, q,
-                       kc, p.T_c, p.n_query, p.H, p.H_kv, G, w.rows_pad, scale, lse, p.q_lse,
+                       kc, kv_strides(p), p.T_c, p.n_query, p.H, p.H_kv, G, w.rows_pad, scale, lse, p.q_lse,
                        part);
     launch_finalize(p, w, ws, scores, st);
     return hipGetLastError();

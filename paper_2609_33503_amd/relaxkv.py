@@ -44,7 +44,8 @@ class Problem(Structure):
                 ("H_kv", c_int32), ("d", c_int32), ("dtype", c_int32),
                 ("softmax_scale", c_float), ("anchor_ratio", c_double),
                 ("q", c_void_p), ("k_cache", c_void_p), ("v_cache", c_void_p),
-                ("q_lse", c_void_p)]
+                ("q_lse", c_void_p), ("kv_stride_layer", c_int64), ("kv_stride_head", c_int64),
+                ("kv_stride_token", c_int64)]
 
 
 class Sets(Structure):
@@ -157,10 +158,32 @@ def _need(t, name, dtype, shape, device):
         raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    _need_shape(t, name, shape)
+
+
+def _need_shape(t, name, shape):
     if t.dim() != len(shape) or any(want is not None and got != want
                                     for got, want in zip(t.shape, shape)):
         want = tuple("*" if x is None else x for x in shape)
         raise ValueError(f"{name} must have shape {want}, got {tuple(t.shape)}")
+
+
+def _need_cache(t, name, dtype, shape, device, strides=None):
+    """A [L][H_kv][T_c][d] cache tensor: like _need, but any strides of the first
+    three dimensions are passed on (the library checks them); d must be
+    contiguous, and with `strides` given the tensor must have exactly those."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the problem's tensors are on {device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    _need_shape(t, name, shape)
+    if t.stride(3) != 1:
+        raise ValueError(f"{name} must have contiguous rows (stride 1 in d)")
+    if strides is not None and tuple(t.stride()[:3]) != tuple(strides):
+        raise ValueError(f"{name} must have the strides {tuple(strides)} of the request's "
+                         f"cache, got {tuple(t.stride()[:3])}")
 
 
 def _nbytes(t):
@@ -177,8 +200,9 @@ class Request:
     """One problem: the descriptor plus the tensors it points at (kept alive).
 
     q        [L][n_query][H][d]   bf16 or f32, CUDA, contiguous
-    k_cache  [L][H_kv][T_c][d]
-    v_cache  [L][H_kv][T_c][d]
+    k_cache  [L][H_kv][T_c][d]    any strides with contiguous rows (e.g. a slice of a
+                                  cache allocated for more tokens); the library checks them
+    v_cache  [L][H_kv][T_c][d]    the same strides as k_cache
     q_lse    optional [L][n_query][H] f32 (natural log)
     """
 
@@ -195,14 +219,15 @@ class Request:
         H_kv, T_c = k_cache.shape[1], k_cache.shape[2]
         self.device = q.device
         _need(q, "q", q.dtype, (L, Qn, H, d), self.device)
-        _need(k_cache, "k_cache", q.dtype, (L, H_kv, T_c, d), self.device)
-        _need(v_cache, "v_cache", q.dtype, (L, H_kv, T_c, d), self.device)
+        _need_cache(k_cache, "k_cache", q.dtype, (L, H_kv, T_c, d), self.device)
+        self.kv_strides = tuple(k_cache.stride()[:3])
+        _need_cache(v_cache, "v_cache", q.dtype, (L, H_kv, T_c, d), self.device, self.kv_strides)
         if q_lse is not None:
             _need(q_lse, "q_lse", torch.float32, (L, Qn, H), self.device)
         self.dtype = q.dtype
         self.tensors = (q, k_cache, v_cache, q_lse)
         self.p = Problem(L, T_c, Qn, H, H_kv, d, dt, float(softmax_scale), float(anchor_ratio),
-                         _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(q_lse))
+                         _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(q_lse), *self.kv_strides)
         _check(lib.relaxkv_validate(ctypes.byref(self.p)), "relaxkv_validate")
         self.L, self.T_c, self.n_query, self.H, self.H_kv, self.d = L, T_c, Qn, H, H_kv, d
         self.k = anchor_count(anchor_ratio, T_c)
@@ -310,17 +335,16 @@ class Request:
                                           _stream(stream)),
                "relaxkv_sparse_attn")
 
-
     def update_cache(self, sets, layer, k_new, v_new, k_cache, v_cache, stream=None):
         """Fresh rows of R_l (k_new/v_new [n][H_kv][d]) into the cache
-        (k_cache/v_cache: [L][H_kv][T_c][d])."""
+        (k_cache/v_cache: [L][H_kv][T_c][d] with the request's cache strides)."""
         self._sets(sets)
         n = k_new.shape[0] if isinstance(k_new, torch.Tensor) and k_new.dim() == 3 else -1
         _need(k_new, "k_new", self.dtype, (n, self.H_kv, self.d), self.device)
         _need(v_new, "v_new", self.dtype, (n, self.H_kv, self.d), self.device)
         cache = (self.L, self.H_kv, self.T_c, self.d)
-        _need(k_cache, "k_cache", self.dtype, cache, self.device)
-        _need(v_cache, "v_cache", self.dtype, cache, self.device)
+        _need_cache(k_cache, "k_cache", self.dtype, cache, self.device, self.kv_strides)
+        _need_cache(v_cache, "v_cache", self.dtype, cache, self.device, self.kv_strides)
         _check(load().relaxkv_update_cache(ctypes.byref(self.p), ctypes.byref(sets.s), int(layer),
                                            _ptr(k_new), _ptr(v_new), int(n), _ptr(k_cache),
                                            _ptr(v_cache), _stream(stream)),
@@ -337,11 +361,12 @@ class Request:
 
     def query_attn(self, layer, k_cache, v_cache, k_q, v_q, out, lse_out=None, ws=None,
                    stream=None):
-        """k_cache/v_cache [L][H_kv][T_c][d]; k_q/v_q [n_query][H_kv][d]; out [n_query][H][d];
+        """k_cache/v_cache [L][H_kv][T_c][d] (the request's cache strides); k_q/v_q
+        [n_query][H_kv][d]; out [n_query][H][d];
         lse_out [n_query][H] f32."""
         cache = (self.L, self.H_kv, self.T_c, self.d)
-        _need(k_cache, "k_cache", self.dtype, cache, self.device)
-        _need(v_cache, "v_cache", self.dtype, cache, self.device)
+        _need_cache(k_cache, "k_cache", self.dtype, cache, self.device, self.kv_strides)
+        _need_cache(v_cache, "v_cache", self.dtype, cache, self.device, self.kv_strides)
         _need(k_q, "k_q", self.dtype, (self.n_query, self.H_kv, self.d), self.device)
         _need(v_q, "v_q", self.dtype, (self.n_query, self.H_kv, self.d), self.device)
         _need(out, "out", self.dtype, (self.n_query, self.H, self.d), self.device)
@@ -360,8 +385,8 @@ class Request:
         """query_attn through the allocation-free entry point (the library's own
         per-GPU scratch; calls that overlap on one GPU race)."""
         cache = (self.L, self.H_kv, self.T_c, self.d)
-        _need(k_cache, "k_cache", self.dtype, cache, self.device)
-        _need(v_cache, "v_cache", self.dtype, cache, self.device)
+        _need_cache(k_cache, "k_cache", self.dtype, cache, self.device, self.kv_strides)
+        _need_cache(v_cache, "v_cache", self.dtype, cache, self.device, self.kv_strides)
         _need(k_q, "k_q", self.dtype, (self.n_query, self.H_kv, self.d), self.device)
         _need(v_q, "v_q", self.dtype, (self.n_query, self.H_kv, self.d), self.device)
         _need(out, "out", self.dtype, (self.n_query, self.H, self.d), self.device)

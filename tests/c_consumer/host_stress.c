@@ -2,7 +2,7 @@
  * Host-side stress of the library for the sanitizer build (test
  * infrastructure): over a grid of problem shapes, from tiny to the limits the
  * header states, it calls every host-only function (validation, size queries,
- * binding, the anchor count) and every compute entry point with an argument
+ * binding, the anchor count, the cache-stride rules) and every compute entry point with an argument
  * that must be rejected before anything is enqueued, and checks the results
  * against the header's rules.  No call reaches a device: every compute call
  * here fails validation.  Built with AddressSanitizer and UndefinedBehavior-
@@ -139,6 +139,66 @@ static void stress_problem(const relaxkv_problem* p0) {
     EXPECT(relaxkv_counts_to_host(NULL, ifake, NULL, NULL) == RELAXKV_EINVAL, "counts null");
 }
 
+/* The cache strides on tiny shapes, against two independent checks: the
+ * header's nesting rule tried over every order of the three dimensions (brute
+ * force instead of the library's sort), and, for every accepted layout, that no
+ * two of the L * H_kv * T_c rows share an element. */
+static void stress_strides(void) {
+    const int64_t cand[] = {0, 64, 128, 192, 256, 320, 384, 448, 512, 768, 1024};
+    const int nc = (int)(sizeof cand / sizeof cand[0]);
+    const int d = 64;
+    long accepted = 0, rejected = 0;
+    for (int L = 1; L <= 3; ++L)
+        for (int Hkv = 1; Hkv <= 3; ++Hkv)
+            for (int T = 1; T <= 3; ++T)
+                for (int a = 0; a < nc; ++a)
+                    for (int b = 0; b < nc; ++b)
+                        for (int c = 0; c < nc; ++c) {
+                            relaxkv_problem p = make(L, T, 4, Hkv, Hkv, d, RELAXKV_DTYPE_BF16, 0.5);
+                            p.kv_stride_layer = cand[a];
+                            p.kv_stride_head = cand[b];
+                            p.kv_stride_token = cand[c];
+                            const int64_t sT = cand[c] ? cand[c] : d;
+                            const int64_t sH = cand[b] ? cand[b] : (int64_t)T * sT;
+                            const int64_t sL = cand[a] ? cand[a] : (int64_t)Hkv * sH;
+                            const int64_t st[3] = {sL, sH, sT}, n[3] = {L, Hkv, T};
+                            static const int perm[6][3] = {{0, 1, 2}, {0, 2, 1}, {1, 0, 2},
+                                                           {1, 2, 0}, {2, 0, 1}, {2, 1, 0}};
+                            int nests = 0;
+                            for (int q = 0; q < 6 && !nests; ++q) {   /* perm[q][0] innermost */
+                                int64_t ext = d;
+                                int ok = 1;
+                                for (int i = 0; i < 3; ++i) {
+                                    const int k = perm[q][i];
+                                    if (n[k] <= 1) continue;
+                                    if (st[k] < ext) { ok = 0; break; }
+                                    ext += (n[k] - 1) * st[k];
+                                }
+                                nests = ok;
+                            }
+                            const relaxkv_status v = relaxkv_validate(&p);
+                            EXPECT(v == (nests ? RELAXKV_OK : RELAXKV_EINVAL),
+                                   "strides %lld %lld %lld at L %d H_kv %d T %d: status %d",
+                                   (long long)cand[a], (long long)cand[b], (long long)cand[c], L,
+                                   Hkv, T, (int)v);
+                            if (v != RELAXKV_OK) { ++rejected; continue; }
+                            ++accepted;
+                            int64_t starts[27];
+                            int m = 0;
+                            for (int l = 0; l < L; ++l)
+                                for (int g = 0; g < Hkv; ++g)
+                                    for (int i = 0; i < T; ++i) starts[m++] = l * sL + g * sH + i * sT;
+                            for (int i = 0; i < m; ++i)
+                                for (int j = i + 1; j < m; ++j) {
+                                    const int64_t gap = starts[i] > starts[j] ? starts[i] - starts[j]
+                                                                              : starts[j] - starts[i];
+                                    EXPECT(gap >= d, "accepted strides %lld %lld %lld overlap",
+                                           (long long)sL, (long long)sH, (long long)sT);
+                                }
+                        }
+    EXPECT(accepted > 1000 && rejected > 1000, "stride sweep %ld / %ld", accepted, rejected);
+}
+
 int main(void) {
     const int Ls[] = {1, 2, 40, 1024, 1025};
     const int Ts[] = {1, 2, 63, 64, 65, 1000, 32768, 1 << 20, (1 << 21) - 1, 1 << 21, 1 << 22,
@@ -162,6 +222,7 @@ int main(void) {
                         stress_problem(&p);
                         ++problems;
                     }
+    stress_strides();
     /* Pointer and descriptor checks. */
     EXPECT(relaxkv_validate(NULL) == RELAXKV_EINVAL, "validate NULL");
     relaxkv_problem p = make(2, 100, 4, 8, 2, 64, RELAXKV_DTYPE_BF16, 0.15);

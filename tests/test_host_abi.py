@@ -59,11 +59,12 @@ def test_anchor_count_rejects(rk, r, T):
 def _problem(rk, **kw):
     base = dict(L=4, T_c=2048, n_query=16, H=8, H_kv=2, d=128, dtype=rk.DTYPE_BF16,
                 softmax_scale=0.0, anchor_ratio=0.15, q=0x1000, k_cache=0x2000, v_cache=0x3000,
-                q_lse=None)
+                q_lse=None, sL=0, sH=0, sT=0)
     base.update(kw)
     return rk.Problem(base["L"], base["T_c"], base["n_query"], base["H"], base["H_kv"],
                       base["d"], base["dtype"], base["softmax_scale"], base["anchor_ratio"],
-                      base["q"], base["k_cache"], base["v_cache"], base["q_lse"])
+                      base["q"], base["k_cache"], base["v_cache"], base["q_lse"],
+                      base["sL"], base["sH"], base["sT"])
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -85,6 +86,42 @@ def _problem(rk, **kw):
 def test_validate(rk, kw, status):
     p = _problem(rk, **kw)
     assert rk.load().relaxkv_validate(ctypes.byref(p)) == status
+
+
+# The cache strides (base problem: L 4, H_kv 2, T_c 2048, d 128; dense strides
+# 524288, 262144, 128).  0 is the dense value; rows may not overlap; rows and
+# pointers 16-byte aligned; bf16 token strides below 2^24 with (T_c - 1) * stride
+# + d < 2^31.
+@pytest.mark.parametrize("kw,status", [
+    ({"sL": 524288, "sH": 262144, "sT": 128}, 0),               # the dense values spelled out
+    ({"sH": 2100 * 128}, 0),                                    # room for 2100 tokens per head
+    ({"sH": 2100 * 128, "sL": 2 * 2100 * 128 + 64}, 0),         # and padding between layers
+    ({"sT": 2 * 128, "sH": 128, "sL": 2048 * 256}, 0),          # [L][T_c][H_kv][d]
+    ({"sT": 2 * 128}, 0),                                       # every other row (K/V interleaved)
+    ({"sL": 128, "sH": 4 * 128, "sT": 8 * 128}, 0),             # [T_c][H_kv][L][d]
+    ({"sT": 64}, -1),                                           # rows overlap
+    ({"sH": 2047 * 128}, -1),                                   # heads overlap
+    ({"sH": 2048 * 128 + 64, "sL": 2 * 2048 * 128}, -1),        # layers overlap
+    ({"sT": 128, "sH": 128, "sL": 2048 * 256}, -1),             # two strides alike
+    ({"sL": -1}, -1), ({"sH": -128}, -1), ({"sT": -128}, -1),
+    ({"sT": 132}, -3),                                          # rows not 16-byte aligned
+    ({"sT": 132, "dtype": 0}, 0),                               # 528 bytes: aligned in fp32
+    ({"sH": 2048 * 128 + 4}, -3),
+    ({"k_cache": 0x2008}, -3), ({"v_cache": 0x3004}, -3), ({"q": 0x1002}, -3),
+    ({"L": 1, "T_c": 2, "sT": 1 << 24}, -3),                    # bf16: 24-bit token offsets
+    ({"L": 1, "T_c": 2, "sT": 1 << 24, "dtype": 0}, 0),
+    ({"L": 1, "T_c": 1 << 14, "sT": (1 << 17) + 8}, -3),        # (T_c - 1) * stride + d >= 2^31
+    ({"L": 1, "T_c": 1 << 14, "sT": 1 << 17}, 0),               # 2^31 - 2^17 + 128
+    ({"L": 1, "H_kv": 1, "H": 1, "sH": 8}, 0),                  # a dimension of size 1 is free
+    ({"L": 2, "sL": 1 << 62}, 0),                               # far apart is fine
+    ({"L": 3, "sL": 1 << 62}, -1),                              # but not past int64
+])
+def test_validate_cache_strides(rk, kw, status):
+    p = _problem(rk, **kw)
+    lib = rk.load()
+    assert lib.relaxkv_validate(ctypes.byref(p)) == status
+    if status != 0:
+        assert lib.relaxkv_sets_bytes(ctypes.byref(p)) == 0
 
 
 @pytest.mark.parametrize("kw,n_split", [
