@@ -221,8 +221,10 @@ int32_t relaxkv_anchor_count(double anchor_ratio, int32_t T_c);
  * of size 1 are ignored),
  * RELAXKV_EUNSUPPORTED for a head_dim, dtype, GQA group or bf16 layer size
  * (see the limits above) this build has no kernel for, a pointer or cache row
- * that is not 16-byte aligned, or (bf16) a token stride of 2^24 elements or
- * more or with (T_c - 1) * stride + d >= RELAXKV_MAX_BF16_LAYER_ELEMS. */
+ * that is not 16-byte aligned, cache strides spanning 2^48 elements or more,
+ * or (bf16, T_c > 1) a token stride of 2^24 elements or more or with
+ * (T_c - 1) * stride + d >= RELAXKV_MAX_BF16_LAYER_ELEMS.  The stride of a
+ * cache dimension of size 1 is never used and not checked. */
 relaxkv_status relaxkv_validate(const relaxkv_problem* p);
 
 /* Host only.  Device scratch bytes relaxkv_score needs (0 when p is invalid). */

@@ -60,38 +60,45 @@ bool sets_match(const relaxkv_problem* p, const relaxkv_sets* s) {
 
 // The cache strides: none negative; no two rows overlap, i.e. taken from the
 // smallest, each stride of a dimension with more than one entry steps past the
-// whole extent of the dimensions inside it; 16-byte aligned rows and pointers
-// (the kernels move rows in 16-byte pieces); and, for bf16, cached-row offsets
-// within a head that fit the attention's 32-bit element offsets.
+// whole extent of the dimensions inside it; an extent below 2^48 elements (no
+// device holds more, and every offset the kernels form then fits in 64 bits);
+// 16-byte aligned rows and pointers (the kernels move rows in 16-byte pieces);
+// and, for bf16, cached-row offsets within a head that fit the attention's
+// 32-bit element offsets.  The stride of a dimension with one entry is never
+// used and is not checked.
 relaxkv_status strides_status(const relaxkv_problem* p) {
     if (p->kv_stride_layer < 0 || p->kv_stride_head < 0 || p->kv_stride_token < 0)
         return RELAXKV_EINVAL;
-    const KvStrides s = kv_strides(*p);
-    struct Dim { int64_t stride, n; } dims[3] = {{s.token, p->T_c}, {s.head, p->H_kv},
-                                                  {s.layer, p->L}};
+    constexpr int64_t kMaxExtent = (int64_t)1 << 48;
+    // The dense defaults (as kv_strides forms them), with overflow checks.
+    int64_t sT = p->kv_stride_token ? p->kv_stride_token : p->d, sH, sL;
+    if (p->kv_stride_head) sH = p->kv_stride_head;
+    else if (__builtin_mul_overflow((int64_t)p->T_c, sT, &sH)) return RELAXKV_EUNSUPPORTED;
+    if (p->kv_stride_layer) sL = p->kv_stride_layer;
+    else if (__builtin_mul_overflow((int64_t)p->H_kv, sH, &sL)) return RELAXKV_EUNSUPPORTED;
+    struct Dim { int64_t stride, n; } dims[3] = {{sT, p->T_c}, {sH, p->H_kv}, {sL, p->L}};
     for (int i = 1; i < 3; ++i)                          // ascending strides (insertion sort)
         for (int j = i; j > 0 && dims[j].stride < dims[j - 1].stride; --j) {
             const Dim t = dims[j];
             dims[j] = dims[j - 1];
             dims[j - 1] = t;
         }
+    const int64_t align = p->dtype == RELAXKV_DTYPE_BF16 ? 8 : 4;   // elements per 16 bytes
     int64_t extent = p->d;                               // elements spanned by the inner dimensions
     for (const Dim& dm : dims) {
         if (dm.n <= 1) continue;
         if (dm.stride < extent) return RELAXKV_EINVAL;
-        // (n - 1) * stride + extent, guarded against int64 overflow
-        if (dm.stride > (INT64_MAX - extent) / (dm.n - 1)) return RELAXKV_EINVAL;
+        if (dm.stride % align) return RELAXKV_EUNSUPPORTED;
+        // extent += (n - 1) * stride, kept below 2^48
+        if (dm.stride > (kMaxExtent - extent) / (dm.n - 1)) return RELAXKV_EUNSUPPORTED;
         extent += (dm.n - 1) * dm.stride;
     }
-    const int64_t esz = p->dtype == RELAXKV_DTYPE_BF16 ? 2 : 4;
-    if ((s.layer * esz) % 16 || (s.head * esz) % 16 || (s.token * esz) % 16)
-        return RELAXKV_EUNSUPPORTED;
     if ((uintptr_t)p->q % 16 || (uintptr_t)p->k_cache % 16 || (uintptr_t)p->v_cache % 16)
         return RELAXKV_EUNSUPPORTED;
     // (the bf16 attention forms the offset with a 24-bit multiply)
-    if (p->dtype == RELAXKV_DTYPE_BF16 &&
-        (s.token >= ((int64_t)1 << 24) ||
-         (int64_t)(p->T_c - 1) * s.token + p->d >= RELAXKV_MAX_BF16_LAYER_ELEMS))
+    if (p->dtype == RELAXKV_DTYPE_BF16 && p->T_c > 1 &&
+        (sT >= ((int64_t)1 << 24) ||
+         (int64_t)(p->T_c - 1) * sT + p->d >= RELAXKV_MAX_BF16_LAYER_ELEMS))
         return RELAXKV_EUNSUPPORTED;
     return RELAXKV_OK;
 }

@@ -181,9 +181,16 @@ def _need_cache(t, name, dtype, shape, device, strides=None):
     _need_shape(t, name, shape)
     if t.stride(3) != 1:
         raise ValueError(f"{name} must have contiguous rows (stride 1 in d)")
-    if strides is not None and tuple(t.stride()[:3]) != tuple(strides):
+    if strides is not None and _cache_strides(t) != tuple(strides):
         raise ValueError(f"{name} must have the strides {tuple(strides)} of the request's "
-                         f"cache, got {tuple(t.stride()[:3])}")
+                         f"cache, got {_cache_strides(t)}")
+
+
+def _cache_strides(t):
+    """The layer, KV-head and token strides of a cache tensor for the descriptor
+    (0, the dense value, for a dimension of size 1, whose stride torch leaves
+    arbitrary and the library never uses)."""
+    return tuple(st if n > 1 else 0 for st, n in zip(t.stride()[:3], t.shape[:3]))
 
 
 def _nbytes(t):
@@ -220,7 +227,7 @@ class Request:
         self.device = q.device
         _need(q, "q", q.dtype, (L, Qn, H, d), self.device)
         _need_cache(k_cache, "k_cache", q.dtype, (L, H_kv, T_c, d), self.device)
-        self.kv_strides = tuple(k_cache.stride()[:3])
+        self.kv_strides = _cache_strides(k_cache)
         _need_cache(v_cache, "v_cache", q.dtype, (L, H_kv, T_c, d), self.device, self.kv_strides)
         if q_lse is not None:
             _need(q_lse, "q_lse", torch.float32, (L, Qn, H), self.device)

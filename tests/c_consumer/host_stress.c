@@ -197,6 +197,19 @@ static void stress_strides(void) {
                                 }
                         }
     EXPECT(accepted > 1000 && rejected > 1000, "stride sweep %ld / %ld", accepted, rejected);
+    /* Strides near the int64 range: refused, with no overflow along the way (UBSan). */
+    const int64_t huge[] = {(int64_t)1 << 47, (int64_t)1 << 48, (int64_t)1 << 62, INT64_MAX - 7,
+                            INT64_MAX};
+    for (int i = 0; i < 5; ++i)
+        for (int which = 0; which < 3; ++which) {
+            relaxkv_problem p = make(40, 32768, 64, 40, 8, 128, RELAXKV_DTYPE_BF16, 0.15);
+            if (which == 0) p.kv_stride_layer = huge[i];
+            if (which == 1) p.kv_stride_head = huge[i];
+            if (which == 2) p.kv_stride_token = huge[i];
+            const relaxkv_status v = relaxkv_validate(&p);
+            EXPECT(v == RELAXKV_EUNSUPPORTED || v == RELAXKV_EINVAL, "huge stride %d/%d: %d", i,
+                   which, (int)v);
+        }
 }
 
 int main(void) {

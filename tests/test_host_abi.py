@@ -113,8 +113,13 @@ def test_validate(rk, kw, status):
     ({"L": 1, "T_c": 1 << 14, "sT": (1 << 17) + 8}, -3),        # (T_c - 1) * stride + d >= 2^31
     ({"L": 1, "T_c": 1 << 14, "sT": 1 << 17}, 0),               # 2^31 - 2^17 + 128
     ({"L": 1, "H_kv": 1, "H": 1, "sH": 8}, 0),                  # a dimension of size 1 is free
-    ({"L": 2, "sL": 1 << 62}, 0),                               # far apart is fine
-    ({"L": 3, "sL": 1 << 62}, -1),                              # but not past int64
+    ({"L": 1, "sL": 3}, 0),                                     # even unaligned
+    ({"L": 1, "T_c": 1, "sT": (1 << 24) + 8}, 0),               # one token: its stride is unused
+    ({"L": 2, "sL": 1 << 40}, 0),                               # far apart is fine
+    ({"L": 2, "sL": 1 << 48}, -3),                              # but not past 2^48 elements
+    ({"L": 3, "sL": 1 << 62}, -3),                              # nor past int64
+    ({"sT": 1 << 62}, -3),                                      # dense head stride T_c * 2^62
+    ({"sH": 1 << 62}, -3),                                      # dense layer stride H_kv * 2^62
 ])
 def test_validate_cache_strides(rk, kw, status):
     p = _problem(rk, **kw)
