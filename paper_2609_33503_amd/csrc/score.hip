@@ -4,10 +4,12 @@
 //
 // bf16 path (bf16 MFMA, fp32 accumulation).  Per layer l and KV head g the
 // Qn*G query rows that share g form one row set.  A workgroup takes one
-// (l, g, split of 4096 contiguous keys): it stages the row set into LDS once
-// (fragment-major), and each of its waves loads its own 32-key blocks from HBM
-// straight into registers and runs every 32-row block against them, so a query
-// fragment read from LDS feeds two MFMAs and K never passes through LDS:
+// (l, g, split of contiguous keys: 4096 in the statistics pass, 4096 or 8192 in
+// the column-sum pass): it stages the row set into LDS once (fragment-major),
+// and each of its waves loads its own 32-key blocks from HBM straight into
+// registers and runs every 32-row block against them, so K never passes
+// through LDS (in the column-sum pass a wave holds two key blocks, so a query
+// fragment read from LDS feeds two MFMAs):
 //   1. score_stats_kreg -- S^T = K Q^T (one query row per lane): each row's
 //      (reference, sum of exp2) over the split.           [skipped with q_lse]
 //   2. score_merge  -- per row, merge the splits into a log2-sum-exp.
@@ -30,13 +32,19 @@ namespace relaxkv {
 namespace {
 
 #ifndef RELAXKV_SCORE_SPLIT
-#define RELAXKV_SCORE_SPLIT 4096              // keys per workgroup
+#define RELAXKV_SCORE_SPLIT 4096              // keys per statistics workgroup
 #endif
 #ifndef RELAXKV_SCORE_KREG_NW
 #define RELAXKV_SCORE_KREG_NW 16              // waves per workgroup (four per SIMD)
 #endif
 #ifndef RELAXKV_SCORE_KREG_NKB
-#define RELAXKV_SCORE_KREG_NKB 1              // 32-key blocks per wave and round
+#define RELAXKV_SCORE_KREG_NKB 1              // 32-key blocks per wave and round (statistics pass)
+#endif
+#ifndef RELAXKV_SCORE_COLSUM_NW
+#define RELAXKV_SCORE_COLSUM_NW 16            // waves per column-sum workgroup
+#endif
+#ifndef RELAXKV_SCORE_COLSUM_NKB
+#define RELAXKV_SCORE_COLSUM_NKB 2            // 32-key blocks per wave and round (column-sum pass)
 #endif
 constexpr int kKeysPerSplit = RELAXKV_SCORE_SPLIT;
 constexpr int kKregRowBlocks = 10;            // 32-row blocks staged per row chunk
@@ -540,6 +548,19 @@ void launch_finalize(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws
     hipLaunchKernelGGL(score_minmax, grid, dim3(256), 0, st, (const float2*)mm, w.n_blk, p.T_c, scores);
 }
 
+// Keys per column-sum workgroup: 4096 or 8192, whichever needs fewer key-steps
+// per CU on the chip's 256 CUs (ceil(workgroups / 256) * split), the larger one
+// on a tie (fewer query stagings and workgroup starts).  Each key's column sum
+// does not depend on the split, so neither do the scores.
+int colsum_split(const relaxkv_problem& p) {
+    constexpr long kCUs = 256;
+    auto cost = [&](long split) {
+        const long wg = (p.T_c + split - 1) / split * (long)p.H_kv * p.L;
+        return (wg + kCUs - 1) / kCUs * split;
+    };
+    return cost(2 * kKeysPerSplit) <= cost(kKeysPerSplit) ? 2 * kKeysPerSplit : kKeysPerSplit;
+}
+
 template <int D>
 void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char* ws,
                         hipStream_t st, float sl2) {
@@ -551,8 +572,9 @@ void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char*
     float* lse2 = (float*)(ws + w.lse_off);
     float2* stats = (float2*)(ws + w.stats_off);
     constexpr int KNW = RELAXKV_SCORE_KREG_NW, KNKB = RELAXKV_SCORE_KREG_NKB;
-    constexpr int kpr = KNW * KNKB * 32;                  // keys of a round
-    static_assert(kKeysPerSplit % kpr == 0, "the statistics splits are the workspace's n_split");
+    constexpr int CNW = RELAXKV_SCORE_COLSUM_NW, CNKB = RELAXKV_SCORE_COLSUM_NKB;
+    static_assert(kKeysPerSplit % (KNW * KNKB * 32) == 0 && kKeysPerSplit % (CNW * CNKB * 32) == 0,
+                  "a split is whole rounds of both passes (the statistics splits are the workspace's n_split)");
     const int kps = kKeysPerSplit;
     const dim3 kgrid((p.T_c + kps - 1) / kps, p.H_kv, p.L);
     if (!p.q_lse) {
@@ -563,8 +585,10 @@ void launch_passes_bf16(const relaxkv_problem& p, const ScoreWorkspace& w, char*
         hipLaunchKernelGGL(score_merge, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                            (const float2*)stats, p.L * p.H_kv, w.n_split, w.rows_pad, n_rows, lse2);
     }
-    hipLaunchKernelGGL((score_colsum_kreg<D, KNW, KNKB>), kgrid, dim3(KNW * 64), 0, st, q, kc,
-                       kv_strides(p), p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, kps, sl2,
+    const int cps = colsum_split(p);
+    const dim3 cgrid((p.T_c + cps - 1) / cps, p.H_kv, p.L);
+    hipLaunchKernelGGL((score_colsum_kreg<D, CNW, CNKB>), cgrid, dim3(CNW * 64), 0, st, q, kc,
+                       kv_strides(p), p.T_c, p.n_query, p.H, p.H_kv, G, n_rows, w.rows_pad, cps, sl2,
                        (const float*)lse2, p.q_lse, part);
 }
 
