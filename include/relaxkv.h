@@ -38,8 +38,10 @@
  *   float32) for Q/K/V and attention outputs.
  * - Layers are 0-based; positions are context positions 0 .. T_c-1 (the
  *   query tokens are never targets or context).
- * - The library keeps no host state between calls and calls are reentrant;
- *   two calls that write the same buffers must be ordered by the caller.
+ * - The library keeps no host state between calls (besides the per-device
+ *   address of relaxkv_query_attn_noalloc's scratch array, looked up once per
+ *   device) and calls are reentrant; two calls that write the same buffers must
+ *   be ordered by the caller.
  *   Device state lives in caller-owned buffers: the sets buffer holds the bf16
  *   attention's work counters (each launch returns its slot to zero), so two
  *   relaxkv_sparse_attn launches with the same sets, layer and context mode
