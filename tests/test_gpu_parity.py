@@ -507,3 +507,30 @@ def test_attention_concurrent_layers_and_modes(gpu_lib):
         O_ref, lse_ref = case.oracle_attn(l, sets_ref, fresh[l], mode=mode)
         assert_close(out.float().cpu().numpy(), O_ref, w, f"O {mode} layer {l}", rel_gate=1e-2)
         assert_close(lse.cpu().numpy(), lse_ref, w, f"lse {mode} layer {l}")
+
+
+def test_colsum_split_does_not_change_scores(gpu_lib):
+    """The column-sum pass takes 4096- or 8192-key splits, whichever needs fewer
+    key-steps per CU for the problem's size; a key's column sum does not depend
+    on the split.  Layer 0 of an 8K context is scored inside a 64-layer problem
+    (8192-key splits) and alone (4096-key splits): the same bits in both scoring
+    modes, and within the bf16 tolerance of the oracle."""
+    w = synth.shrink(synth.WORKLOADS["llama8b-8k"], L=64)
+    q, kc, vc = synth.make_cache(w, "cuda")
+    g = torch.Generator(device="cuda").manual_seed(7)
+    lse = (torch.randn(w.L, w.Qn, w.H, device="cuda", generator=g) * 0.1
+           + math.log(w.T_c)).float()
+
+    def scores(n_layers, q_lse):
+        req = relaxkv.Request(q[:n_layers], kc[:n_layers], vc[:n_layers], w.ratio,
+                              q_lse=None if q_lse is None else q_lse[:n_layers])
+        a = torch.empty(n_layers, w.T_c, dtype=torch.float32, device="cuda")
+        req.score(req.alloc_workspace(), a)
+        torch.cuda.synchronize()
+        return a[0].cpu()
+
+    for q_lse in (None, lse):
+        a_all, a_one = scores(w.L, q_lse), scores(1, q_lse)
+        assert torch.equal(a_all, a_one), "one-pass" if q_lse is not None else "self-contained"
+    a_ref, _, _ = oracle.score(synth.to_f64(q[:1]), synth.to_f64(kc[:1]))
+    assert_close(scores(1, None).numpy(), a_ref[0], w, "layer 0 self-contained scores")
