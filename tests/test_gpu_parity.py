@@ -534,3 +534,31 @@ def test_colsum_split_does_not_change_scores(gpu_lib):
         assert torch.equal(a_all, a_one), "one-pass" if q_lse is not None else "self-contained"
     a_ref, _, _ = oracle.score(synth.to_f64(q[:1]), synth.to_f64(kc[:1]))
     assert_close(scores(1, None).numpy(), a_ref[0], w, "layer 0 self-contained scores")
+
+
+def test_maximum_bf16_context(gpu_lib):
+    """The longest bf16 context the attention takes at 8 KV heads of d 128:
+    T_c = 2^21 - 1, so one layer's cache slab is 2^31 - 1024 elements, just under
+    the 32-bit element offsets of its fills (fresh rank x H_kv d and position x d).
+    Two layers at a 1e-4 anchor ratio (210 anchors each): the scores of both layers
+    against the oracle, selection and every set bit-exact on shared fp32 scores,
+    and every target and head of both layers in both context modes checked by the
+    softmax property (layer 1's union contexts read cached rows of layer-0 anchors
+    anywhere in the 2M positions; the full prefix reads every cached row)."""
+    w = synth.shrink(W["llama8b-8k"], L=2, T_c=(1 << 21) - 1, H=8, H_kv=8, Qn=2, ratio=1e-4)
+    case = Case(w)
+    assert case.k == 210
+    a_gpu = case.gpu_scores().cpu().numpy()
+    a_ref = np.empty((w.L, w.T_c))
+    for l in range(w.L):
+        a_ref[l] = oracle.score(synth.to_f64(case.q[l:l + 1]), synth.to_f64(case.kc[l:l + 1]))[0][0]
+    assert_close(a_gpu, a_ref, w, "scores")
+    a32 = a_ref.astype(np.float32)
+    anchors = case.gpu_select(torch.from_numpy(a32).cuda())
+    anchors_ref = oracle.select(a32.astype(np.float64), case.k)
+    assert np.array_equal(anchors, anchors_ref)
+    sets_ref = oracle.build_sets(anchors_ref, case.T)
+    compare_sets(case.gpu_sets(), sets_ref)
+    for l in range(w.L):
+        for mode in ("union", "full"):
+            every_target_property(case, sets_ref, l, mode)
