@@ -562,3 +562,36 @@ def test_maximum_bf16_context(gpu_lib):
     for l in range(w.L):
         for mode in ("union", "full"):
             every_target_property(case, sets_ref, l, mode)
+
+
+def test_maximum_bf16_context_query_and_update(gpu_lib):
+    """At the same longest bf16 context (T_c = 2^21 - 1, 8 KV heads, d 128): the
+    query-side completion of layer 0 against the oracle, and the cache update of
+    layer 1 in place: the rows of R_1 take the fresh keys and values (at cached
+    offsets up to the end of the slab) and every other row and layer keeps its bits."""
+    from test_gpu_query_attn import oracle_query, run_query
+    w = synth.shrink(W["llama8b-8k"], L=2, T_c=(1 << 21) - 1, H=8, H_kv=8, Qn=2, ratio=1e-4)
+    case = Case(w)
+    kq, vq, out, lse = run_query(case, 0)
+    O_ref, lse_ref = oracle_query(case, 0, kq, vq)
+    assert_close(out.float().cpu().numpy(), O_ref, w, "query-side O", rel_gate=1e-2)
+    assert_close(lse.cpu().numpy(), lse_ref, w, "query-side lse")
+    del O_ref, lse_ref
+
+    case.gpu_select(case.gpu_scores())
+    got = case.gpu_sets()
+    R_1 = got["R"][1]
+    assert len(R_1) == case.k
+    _, kn, vn = case.fresh(1, R_1)
+    kc0, vc0 = case.kc.clone(), case.vc.clone()
+    case.req.update_cache(case.sets, 1, kn, vn, case.kc, case.vc)
+    torch.cuda.synchronize()
+    idx = torch.as_tensor(R_1, dtype=torch.int64, device="cuda")
+    assert torch.equal(case.kc[1].index_select(1, idx), kn.transpose(0, 1))
+    assert torch.equal(case.vc[1].index_select(1, idx), vn.transpose(0, 1))
+    keep = torch.ones(w.T_c, dtype=torch.bool, device="cuda")
+    keep[idx] = False
+    for new, old in ((case.kc, kc0), (case.vc, vc0)):
+        assert torch.equal(new[0], old[0])
+        assert torch.equal(new[1][:, keep], old[1][:, keep])
+    assert int(R_1.max()) > (1 << 20)               # rows in the upper half of the slab were written
