@@ -211,8 +211,12 @@ def every_target_property(case, sets_ref, l, mode, n_rows=None):
     keep = torch.as_tensor(~empty, device="cuda")
     keys = torch.arange(len(ctx), device="cuda")
     worst_sum, worst_o, worst_rel = 0.0, 0.0, 0.0
-    for t0 in range(0, n, 256):
-        t1 = min(n, t0 + 256)
+    # Targets per block: the fp32 logits of a block ([c*G][|ctx|]) stay below
+    # 2^31 bytes, past which torch's fp32 matmul/reduction path on this stack
+    # returned wrong rows (seen at a 4M-key context: every row past byte 2^31).
+    step = max(1, min(256, ((1 << 29) - 1) // (G * len(ctx))))
+    for t0 in range(0, n, step):
+        t1 = min(n, t0 + step)
         k_rows = keep[t0:t1]
         if not bool(k_rows.any()):
             continue

@@ -536,7 +536,14 @@ def test_colsum_split_does_not_change_scores(gpu_lib):
     assert_close(scores(1, None).numpy(), a_ref[0], w, "layer 0 self-contained scores")
 
 
-def test_maximum_bf16_context(gpu_lib):
+# The longest bf16 contexts: the slab bound at 8 KV heads of d 128, and the
+# context-length bound itself (T_c = 2^22) at 2 KV heads.
+MAX_SHAPES = {"slab": dict(T_c=(1 << 21) - 1, H=8, H_kv=8, ratio=1e-4),
+              "context": dict(T_c=1 << 22, H=2, H_kv=2, ratio=5e-5)}
+
+
+@pytest.mark.parametrize("shape", list(MAX_SHAPES))
+def test_maximum_bf16_context(gpu_lib, shape):
     """The longest bf16 context the attention takes at 8 KV heads of d 128:
     T_c = 2^21 - 1, so one layer's cache slab is 2^31 - 1024 elements, just under
     the 32-bit element offsets of its fills (fresh rank x H_kv d and position x d).
@@ -545,7 +552,7 @@ def test_maximum_bf16_context(gpu_lib):
     and every target and head of both layers in both context modes checked by the
     softmax property (layer 1's union contexts read cached rows of layer-0 anchors
     anywhere in the 2M positions; the full prefix reads every cached row)."""
-    w = synth.shrink(W["llama8b-8k"], L=2, T_c=(1 << 21) - 1, H=8, H_kv=8, Qn=2, ratio=1e-4)
+    w = synth.shrink(W["llama8b-8k"], L=2, Qn=2, **MAX_SHAPES[shape])
     case = Case(w)
     assert case.k == 210
     a_gpu = case.gpu_scores().cpu().numpy()
@@ -564,13 +571,14 @@ def test_maximum_bf16_context(gpu_lib):
             every_target_property(case, sets_ref, l, mode)
 
 
-def test_maximum_bf16_context_query_and_update(gpu_lib):
-    """At the same longest bf16 context (T_c = 2^21 - 1, 8 KV heads, d 128): the
+@pytest.mark.parametrize("shape", list(MAX_SHAPES))
+def test_maximum_bf16_context_query_and_update(gpu_lib, shape):
+    """At the same longest bf16 contexts (T_c = 2^21 - 1 at 8 KV heads, 2^22 at 2): the
     query-side completion of layer 0 against the oracle, and the cache update of
     layer 1 in place: the rows of R_1 take the fresh keys and values (at cached
     offsets up to the end of the slab) and every other row and layer keeps its bits."""
     from test_gpu_query_attn import oracle_query, run_query
-    w = synth.shrink(W["llama8b-8k"], L=2, T_c=(1 << 21) - 1, H=8, H_kv=8, Qn=2, ratio=1e-4)
+    w = synth.shrink(W["llama8b-8k"], L=2, Qn=2, **MAX_SHAPES[shape])
     case = Case(w)
     kq, vq, out, lse = run_query(case, 0)
     O_ref, lse_ref = oracle_query(case, 0, kq, vq)
@@ -594,4 +602,4 @@ def test_maximum_bf16_context_query_and_update(gpu_lib):
     for new, old in ((case.kc, kc0), (case.vc, vc0)):
         assert torch.equal(new[0], old[0])
         assert torch.equal(new[1][:, keep], old[1][:, keep])
-    assert int(R_1.max()) > (1 << 20)               # rows in the upper half of the slab were written
+    assert int(R_1.max()) > w.T_c // 2              # rows in the upper half of the slab were written
